@@ -1,0 +1,375 @@
+"""CPU ORACLE -- test infrastructure only (see the package docstring).
+
+The decoding loop of self-speculative decoding with a learned (exit layer,
+draft length) policy, written plainly in fp64 on top of ``lede_oracle.c``.
+
+Paper references: Section 1 and 2.2 (self-speculative decoding: early layers
+draft, the full model verifies in parallel); Section 3.1 (the MDP: a state
+from the hidden state at a candidate exit layer, an action, the reward of
+Section 3.1.3); Section 3.2 (greedy action from a small MLP Q-network);
+Section 3.3 (exit layer chosen during the first forward pass of a step, then
+drafting at that layer); Section 4.1 (batch 1, greedy decoding, speculative
+acceptance, metrics E, d, acceptance rate).
+
+Readings where the paper is silent (each is also listed in the design notes):
+* the early-exit head is the shared final RMSNorm + LM head;
+* acceptance is greedy: the longest prefix of drafts equal to the full
+  model's argmax, plus the full model's token after it (the bonus token);
+* verification recomputes all L layers for the k+1 rows and overwrites the
+  drafted KV; positions past the committed length are discarded;
+* the Q-network reads the final-normed hidden state of the pending token at
+  the smallest candidate exit layer and scores the joint (exit, length) grid;
+* argmax ties go to the lowest index; no EOS: exactly N tokens are produced,
+  with k clamped to N - n_gen - 1;
+* the reward is summed over the drafts up to and including the first
+  rejected one; continue penalties do not arise with a joint action.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from collections import deque
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+from .build import build, library_path
+
+_lib = None
+
+
+class _OracleModel(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int), ("d", ctypes.c_int), ("nq", ctypes.c_int),
+        ("nkv", ctypes.c_int), ("hd", ctypes.c_int), ("ffn", ctypes.c_int),
+        ("vocab", ctypes.c_int), ("is_bf16", ctypes.c_int), ("max_ctx", ctypes.c_int),
+        ("eps", ctypes.c_double), ("rope_base", ctypes.c_double),
+        ("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p), ("head", ctypes.c_void_p),
+        ("attn_norm", ctypes.POINTER(ctypes.c_void_p)), ("wq", ctypes.POINTER(ctypes.c_void_p)),
+        ("wk", ctypes.POINTER(ctypes.c_void_p)), ("wv", ctypes.POINTER(ctypes.c_void_p)),
+        ("wo", ctypes.POINTER(ctypes.c_void_p)), ("ffn_norm", ctypes.POINTER(ctypes.c_void_p)),
+        ("wg", ctypes.POINTER(ctypes.c_void_p)), ("wu", ctypes.POINTER(ctypes.c_void_p)),
+        ("wd", ctypes.POINTER(ctypes.c_void_p)),
+        ("kcache", ctypes.c_void_p), ("vcache", ctypes.c_void_p),
+    ]
+
+
+def lib(path: Optional[str] = None):
+    """The oracle C library (built on first use).  ``path`` loads another
+    build of it (the tests use this to load deliberately broken copies)."""
+    global _lib
+    if path is not None:
+        return _bind(ctypes.CDLL(path))
+    if _lib is None:
+        build()
+        _lib = _bind(ctypes.CDLL(library_path()))
+    return _lib
+
+
+def _bind(L):
+    vp, i, d = ctypes.c_void_p, ctypes.c_int, ctypes.c_double
+    L.oracle_forward.argtypes = [ctypes.POINTER(_OracleModel), vp, i, i, i, vp]
+    L.oracle_forward.restype = i
+    L.oracle_head.argtypes = [ctypes.POINTER(_OracleModel), vp, i, vp, vp]
+    L.oracle_head.restype = i
+    L.oracle_linear_f32.argtypes = [vp, vp, i, i, vp, vp]
+    L.oracle_rope.argtypes = [vp, i, i, d]
+    L.oracle_rmsnorm_f64.argtypes = [vp, vp, i, d, vp]
+    L.oracle_attend.argtypes = [vp, vp, vp, i, i, vp, vp]
+    L.oracle_round_bf16.argtypes = [d]
+    L.oracle_round_bf16.restype = d
+    return L
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+class OracleDecoder:
+    """fp64 decoder with a position-indexed KV cache.
+
+    ``weights`` is the dict from ``lede_inputs.weights`` (logical row-major
+    arrays; bf16 as uint16).  ``qnet`` is the dict from
+    ``lede_inputs.qnet_weights`` or None.
+    """
+
+    def __init__(self, model, weights: dict, max_ctx: int, qnet: Optional[dict] = None,
+                 library=None):
+        self.m = model
+        self.w = weights
+        self.qnet_w = qnet
+        self.max_ctx = max_ctx
+        self.L = library if library is not None else lib()
+        kvd = model.n_kv_heads * model.head_dim
+        self.kcache = np.zeros((model.n_layers, max_ctx, kvd), dtype=np.float64)
+        self.vcache = np.zeros((model.n_layers, max_ctx, kvd), dtype=np.float64)
+        n = model.n_layers
+        arr = ctypes.c_void_p * n
+
+        def per_layer(name):
+            return arr(*[_ptr(weights["layers"][j][name]) for j in range(n)])
+
+        self._keep = {name: per_layer(name) for name in
+                      ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")}
+        s = _OracleModel()
+        s.n_layers, s.d, s.nq, s.nkv = n, model.d_model, model.n_heads, model.n_kv_heads
+        s.hd, s.ffn, s.vocab = model.head_dim, model.ffn_dim, model.vocab
+        s.is_bf16 = 1 if model.dtype == "bf16" else 0
+        s.max_ctx, s.eps, s.rope_base = max_ctx, model.rms_eps, model.rope_base
+        s.embed, s.final_norm, s.head = _ptr(weights["embed"]), _ptr(weights["final_norm"]), _ptr(weights["head"])
+        for name, a in self._keep.items():
+            setattr(s, name, ctypes.cast(a, ctypes.POINTER(ctypes.c_void_p)))
+        s.kcache, s.vcache = _ptr(self.kcache), _ptr(self.vcache)
+        self.s = s
+
+    # -- decoder -----------------------------------------------------------
+    def forward(self, tokens: Sequence[int], pos0: int, l_end: int) -> np.ndarray:
+        """Hidden states [T][d] after layers [0, l_end) of tokens at positions
+        pos0..pos0+T-1; writes their KV for those layers."""
+        toks = np.ascontiguousarray(tokens, dtype=np.int32)
+        out = np.empty((len(toks), self.m.d_model), dtype=np.float64)
+        rc = self.L.oracle_forward(ctypes.byref(self.s), _ptr(toks), len(toks), pos0, l_end, _ptr(out))
+        if rc != 0:
+            raise ValueError("oracle_forward rejected its arguments")
+        return out
+
+    def head(self, hidden: np.ndarray, with_normed: bool = False):
+        """Logits [T][V] of the shared final RMSNorm + LM head."""
+        h = np.ascontiguousarray(hidden, dtype=np.float64)
+        T = h.shape[0]
+        logits = np.empty((T, self.m.vocab), dtype=np.float64)
+        normed = np.empty_like(h) if with_normed else None
+        rc = self.L.oracle_head(ctypes.byref(self.s), _ptr(h), T, _ptr(logits),
+                                _ptr(normed) if with_normed else None)
+        if rc != 0:
+            raise ValueError("oracle_head failed")
+        return (logits, normed) if with_normed else logits
+
+    def qnet(self, state: np.ndarray) -> np.ndarray:
+        """Q-values over the joint (exit, length) grid: W2 ReLU(W1 s + b1) + b2
+        (Section 3.2: a small MLP; greedy action = argmax)."""
+        q = self.qnet_w
+        s = np.ascontiguousarray(state, dtype=np.float64)
+        hdim = q["w1"].shape[0]
+        hid = np.empty(hdim, dtype=np.float64)
+        self.L.oracle_linear_f32(_ptr(q["w1"]), _ptr(q["b1"]), hdim, s.shape[0], _ptr(s), _ptr(hid))
+        hid = np.maximum(hid, 0.0)
+        out = np.empty(q["w2"].shape[0], dtype=np.float64)
+        self.L.oracle_linear_f32(_ptr(q["w2"]), _ptr(q["b2"]), out.shape[0], hdim, _ptr(hid), _ptr(out))
+        return out
+
+    def qnet_state(self, token: int, pos: int, l_min: int) -> np.ndarray:
+        """Final-RMSNorm'd layer-l_min hidden state of `token` at `pos` (the
+        Q-network's observation; not rounded)."""
+        h = self.forward([token], pos, l_min)
+        _, normed = self.head(h, with_normed=True)
+        return normed[0]
+
+
+def argmax_lowest(z: np.ndarray) -> int:
+    """Index of the maximum, lowest index on ties."""
+    return int(np.argmax(z))  # numpy returns the first occurrence
+
+
+@dataclass
+class ArgmaxInfo:
+    token: int
+    top: float
+    second: float
+    lo: float
+
+    @property
+    def margin(self) -> float:
+        return self.top - self.second
+
+    @property
+    def span(self) -> float:
+        return self.top - self.lo
+
+
+def argmax_info(z: np.ndarray) -> ArgmaxInfo:
+    t = argmax_lowest(z)
+    top = float(z[t])
+    rest = np.delete(z, t)
+    return ArgmaxInfo(t, top, float(rest.max()) if rest.size else -math.inf, float(z.min()))
+
+
+@dataclass
+class Tolerance:
+    """Logit tolerance: absolute for fp32 models, relative to the row's logit
+    range for bf16 models."""
+    abs_f32: float = 1e-4
+    rel_bf16: float = 2e-2
+
+    def of(self, dtype: str, span: float) -> float:
+        return self.abs_f32 if dtype == "f32" else self.rel_bf16 * span
+
+
+def accept_length(drafts: Sequence[int], verify: Sequence[int]) -> int:
+    """Greedy acceptance: largest a <= k with drafts[m] == verify[m] for all
+    m < a (drafts[m] is d_{m+1}, verify[m] is the full model's token after
+    the m-th verify row)."""
+    a = 0
+    while a < len(drafts) and drafts[a] == verify[a]:
+        a += 1
+    return a
+
+
+def reward(a: int, k_eff: int, l_star: int, n_layers: int) -> float:
+    """Section 3.1.3: each accepted draft earns 1 + (L - l*)/L, the first
+    rejected draft earns -2 + (L - l*)/L; later drafts are not scored."""
+    if k_eff == 0:
+        return 0.0
+    lam = (n_layers - l_star) / n_layers
+    return a * (1.0 + lam) + (0.0 if a == k_eff else (-2.0 + lam))
+
+
+class Pager:
+    """Page allocator of the paged KV cache (the paper is silent; this is the
+    reading both implementations follow).  Page size S; a free list seeded
+    with an order; allocation pops the front; truncation frees the pages
+    wholly past the new length and pushes them back to the front in
+    descending logical order, so they are reused in the same order."""
+
+    def __init__(self, n_pages: int, page_size: int, order: Optional[Sequence[int]] = None):
+        self.S = page_size
+        self.free = deque(range(n_pages) if order is None else order)
+        self.table: List[int] = []
+
+    def ensure(self, n_positions: int):
+        while len(self.table) * self.S < n_positions:
+            if not self.free:
+                raise MemoryError("KV pool exhausted")
+            self.table.append(self.free.popleft())
+
+    def truncate(self, new_len: int):
+        keep = -(-new_len // self.S)
+        for j in range(len(self.table) - 1, keep - 1, -1):
+            self.free.appendleft(self.table[j])
+        self.table = self.table[:keep]
+
+
+@dataclass
+class StepRecord:
+    l: int
+    k_req: int
+    k_eff: int
+    accepted: int
+    emitted: List[int]
+    drafts: List[int]
+    verify: List[int]
+    reward: float
+    seq_len: int
+    q_action: int = -1
+    q_values: Optional[np.ndarray] = None
+    draft_info: List[ArgmaxInfo] = field(default_factory=list)
+    verify_info: List[ArgmaxInfo] = field(default_factory=list)
+    block_table: List[int] = field(default_factory=list)
+
+
+def greedy_ar(dec: OracleDecoder, prompt: Sequence[int], n_gen: int):
+    """Plain greedy autoregressive decoding of the full model: the result the
+    self-speculative loop must reproduce exactly.  Returns (tokens, infos)."""
+    L = dec.m.n_layers
+    h = dec.forward(prompt, 0, L)
+    info = argmax_info(dec.head(h[-1:])[0])
+    toks, infos = [info.token], [info]
+    pos = len(prompt)
+    while len(toks) < n_gen:
+        h = dec.forward([toks[-1]], pos, L)
+        pos += 1
+        info = argmax_info(dec.head(h)[0])
+        toks.append(info.token)
+        infos.append(info)
+    return toks, infos
+
+
+class SSDState:
+    """(c, pending token, n_gen) plus the pager and the committed output."""
+
+    def __init__(self, dec: OracleDecoder, n_pages: int, page_size: int, order=None):
+        self.dec = dec
+        self.pager = Pager(n_pages, page_size, order)
+        self.c = 0
+        self.pending = -1
+        self.out: List[int] = []
+
+    def prefill(self, prompt: Sequence[int]) -> ArgmaxInfo:
+        self.pager.ensure(len(prompt))
+        h = self.dec.forward(prompt, 0, self.dec.m.n_layers)
+        info = argmax_info(self.dec.head(h[-1:])[0])
+        self.c = len(prompt)
+        self.pending = info.token
+        self.out = [info.token]
+        return info
+
+    def step(self, l: int, k: int, n_total: int, qnet: bool = False, use_qnet_action: bool = False) -> StepRecord:
+        """One draft / verify / accept / commit step (Sections 2.2, 3.3)."""
+        dec, m = self.dec, self.dec.m
+        L = m.n_layers
+        n_gen = len(self.out)
+        k_eff = max(0, min(k, n_total - n_gen - 1))
+        q_values, q_action = None, -1
+        if qnet and k_eff > 0:
+            l_min = min(m.exits)
+            q_values = dec.qnet(dec.qnet_state(self.pending, self.c, l_min))
+            q_action = argmax_lowest(q_values)
+            if use_qnet_action:
+                l = m.exits[q_action // len(m.lengths)]
+                k = m.lengths[q_action % len(m.lengths)]
+                k_eff = max(0, min(k, n_total - n_gen - 1))
+        if not 1 <= l <= L:
+            raise ValueError("exit layer out of range")
+        self.pager.ensure(self.c + k_eff + 1)
+        drafts, dinfo = [], []
+        u = self.pending
+        for i in range(1, k_eff + 1):
+            h = dec.forward([u], self.c + i - 1, l)
+            info = argmax_info(dec.head(h)[0])
+            drafts.append(info.token)
+            dinfo.append(info)
+            u = info.token
+        h = dec.forward([self.pending] + drafts, self.c, L)
+        z = dec.head(h)
+        vinfo = [argmax_info(z[i]) for i in range(k_eff + 1)]
+        verify = [v.token for v in vinfo]
+        a = accept_length(drafts, verify)
+        emitted = drafts[:a] + [verify[a]]
+        self.c += a + 1
+        self.pending = verify[a]
+        self.out.extend(emitted)
+        self.pager.truncate(self.c)
+        return StepRecord(l=l, k_req=k, k_eff=k_eff, accepted=a, emitted=emitted, drafts=drafts,
+                          verify=verify, reward=reward(a, k_eff, l, L), seq_len=self.c,
+                          q_action=q_action, q_values=q_values, draft_info=dinfo, verify_info=vinfo,
+                          block_table=list(self.pager.table))
+
+
+def ssd_generate(dec: OracleDecoder, prompt: Sequence[int], n_total: int, actions, n_pages: int,
+                 page_size: int = 64, qnet: bool = False, use_qnet_action: bool = False):
+    """Self-speculative greedy generation of n_total tokens.  ``actions`` is a
+    sequence of (l, k) per step (ignored for the action when
+    use_qnet_action).  Returns (state, records)."""
+    st = SSDState(dec, n_pages, page_size)
+    st.prefill(prompt)
+    recs = []
+    i = 0
+    while len(st.out) < n_total:
+        l, k = actions[min(i, len(actions) - 1)]
+        recs.append(st.step(int(l), int(k), n_total, qnet=qnet, use_qnet_action=use_qnet_action))
+        i += 1
+    return st, recs
+
+
+def metrics(records: Sequence[StepRecord]) -> dict:
+    """Section 4.1 metrics over steps that drafted: E (mean exit layer),
+    d (mean draft length), acceptance rate (accepted / drafted)."""
+    drafted = [r for r in records if r.k_eff > 0]
+    if not drafted:
+        return {"E": float("nan"), "d": float("nan"), "acc": float("nan"), "steps": len(records)}
+    return {"E": sum(r.l for r in drafted) / len(drafted),
+            "d": sum(r.k_eff for r in drafted) / len(drafted),
+            "acc": sum(r.accepted for r in drafted) / sum(r.k_eff for r in drafted),
+            "steps": len(records),
+            "tokens": sum(len(r.emitted) for r in records)}

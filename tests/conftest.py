@@ -1,0 +1,21 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
+    config.addinivalue_line("markers", "slow: full-size model; minutes of host work")
+
+
+def pytest_collection_modifyitems(config, items):
+    # GPU tests print what they run before each GPU step, so a failing box
+    # still names its case.
+    for item in items:
+        if "gpu" in item.keywords:
+            item.add_marker(pytest.mark.timeout(900))
