@@ -1,0 +1,216 @@
+/*
+ * liblede -- batch-1 self-speculative decoding with learned (exit layer,
+ * draft length) control, for AMD Instinct MI355X (gfx950).
+ *
+ * The method (Zhu et al., "Experience-Driven Dynamic Exits for LLMs with
+ * Reinforcement Learning"): the model's own first l* layers draft k tokens,
+ * each read out through the shared final RMSNorm and LM head (Section 2.2;
+ * Section 3.1.1 -- the next-token distribution at layer l is computed from
+ * the layer-l hidden state); the full L-layer model then verifies the k
+ * drafts in one parallel pass (Section 1); a small MLP Q-network chooses
+ * (l*, k) inside the loop (Sections 3.2, 3.3).  Decoding is greedy
+ * (Section 4.1): the longest prefix of drafts equal to the full model's
+ * argmax is accepted, followed by the full model's own next token.
+ *
+ * Conventions for every entry point:
+ *  - Return value: LEDE_OK (0) or a negative lede_status.  On error the
+ *    decoding state (KV length, pending token, page table) is unchanged and
+ *    lede_last_error() describes the failure.  No exception crosses the ABI.
+ *  - Device pointers are HIP device addresses on the current device; host
+ *    pointers are ordinary process memory.  The caller owns every buffer it
+ *    passes (weights staging, weight arena, KV pool, workspace) and the
+ *    stream; the library owns only its host-side context.  No hot call
+ *    allocates device memory.
+ *  - `stream` is a hipStream_t passed as void*.  All device work is ordered
+ *    on it.  Calls that return host values synchronise the stream.
+ *  - A context is used by one host thread at a time.
+ *
+ * Model: Llama-style decoder -- RMSNorm, rotary position embedding
+ * (rotate-half pairs (i, i + hd/2), angle pos * base^(-2i/hd)), grouped-query
+ * attention (query head h reads KV head h / (n_heads / n_kv_heads)), SwiGLU
+ * feed-forward, untied LM head.  Weights are bf16 or fp32; for bf16 models
+ * the inputs of every linear layer and the cached K/V are rounded to bf16
+ * (nearest-even) and everything else is accumulated in fp32.
+ */
+#ifndef LEDE_H
+#define LEDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lede_ctx lede_ctx;
+
+typedef enum {
+  LEDE_OK = 0,
+  LEDE_E_ARG = -1,           /* bad argument: null pointer, size, range */
+  LEDE_E_STATE = -2,         /* call not valid in the current decoding state */
+  LEDE_E_KV_FULL = -3,       /* no free KV page left in the pool */
+  LEDE_E_CTX_OVERFLOW = -4,  /* position would exceed max_ctx */
+  LEDE_E_HIP = -5,           /* a HIP runtime call failed */
+  LEDE_E_UNSUPPORTED = -6    /* shape outside what the kernels handle */
+} lede_status;
+
+enum { LEDE_DTYPE_F32 = 0, LEDE_DTYPE_BF16 = 1 };
+
+/* Model shape, KV pool geometry and the Q-network's action grid. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps;     /* RMSNorm epsilon */
+  float rope_base;   /* rotary base (10000, 500000, ...) */
+  int32_t dtype;     /* LEDE_DTYPE_F32 or LEDE_DTYPE_BF16 */
+  int32_t max_ctx;   /* largest KV length (positions) a sequence may reach */
+  int32_t page_size; /* tokens per KV page; must be 64 */
+  int32_t n_pages;   /* pages in the KV pool */
+  int32_t qnet_hidden;         /* Q-network hidden width H (0: no Q-network) */
+  int32_t n_exits, n_lengths;  /* action grid E x K, row-major (exit major) */
+  int32_t exits[64];           /* candidate exit layers, ascending, 1..n_layers */
+  int32_t lengths[16];         /* candidate draft lengths, 1..16 */
+  int32_t k_max;               /* largest draft length any call may use (<= 15) */
+} lede_config;
+
+/* Tensor kinds for lede_load_tensor.  Logical layouts (row-major [out][in]):
+ * EMBED, HEAD [vocab][d]; FINAL_NORM, ATTN_NORM, FFN_NORM [d];
+ * WQ [n_heads*hd][d]; WK, WV [n_kv*hd][d]; WO [d][n_heads*hd];
+ * WG, WU [ffn][d]; WD [d][ffn]; all in the model dtype.
+ * QNET_W1 [H][d], QNET_B1 [H], QNET_W2 [E*K][H], QNET_B2 [E*K]: fp32. */
+typedef enum {
+  LEDE_T_EMBED = 0, LEDE_T_FINAL_NORM, LEDE_T_HEAD,
+  LEDE_T_ATTN_NORM, LEDE_T_WQ, LEDE_T_WK, LEDE_T_WV, LEDE_T_WO,
+  LEDE_T_FFN_NORM, LEDE_T_WG, LEDE_T_WU, LEDE_T_WD,
+  LEDE_T_QNET_W1, LEDE_T_QNET_B1, LEDE_T_QNET_W2, LEDE_T_QNET_B2
+} lede_tensor;
+
+/* An action of the agent: exit layer l* (1..L) and draft length k. */
+typedef struct {
+  int32_t l, k;
+} lede_action;
+
+/* One logged transition (Section 3.2 stores (s, a, r, s') tuples): the
+ * action, what verification accepted, the tokens committed and the
+ * Section 3.1.3 reward summed over the step's scored drafts. */
+typedef struct {
+  int32_t l;           /* exit layer used */
+  int32_t k_req;       /* requested draft length */
+  int32_t k_eff;       /* draft length after clamping to the tokens left */
+  int32_t accepted;    /* accepted drafts a (0..k_eff) */
+  int32_t n_emitted;   /* a + 1 */
+  int32_t tokens[17];  /* committed tokens d_1..d_a, then the verify token */
+  int32_t drafts[16];  /* the k_eff draft tokens */
+  int32_t q_action;    /* argmax index of the Q-network (-1 if not run) */
+  float q_max;         /* its Q-value */
+  float reward;        /* Section 3.1.3 reward of this step */
+  int32_t seq_len;     /* committed KV length after the step */
+  int32_t pending;     /* next pending token (not yet in the cache) */
+} lede_step_record;
+
+/* Bytes of the three device regions the caller allocates for `cfg`:
+ * the weight arena (repacked weights), the KV pool and the workspace.
+ * Returns LEDE_E_UNSUPPORTED for shapes the kernels do not handle
+ * (head_dim not 64/128, d_model or q_dim not a multiple of 32, ffn_dim not
+ * a multiple of 8, page_size != 64, k_max > 15, ...). */
+int lede_region_bytes(const lede_config* cfg, size_t* weight_bytes, size_t* kv_bytes,
+                      size_t* workspace_bytes);
+
+/* Create a context on the current device over caller-owned regions of at
+ * least the sizes above (256-byte aligned).  Uploads the RoPE table to the
+ * workspace (synchronous).  The page free list starts as 0..n_pages-1. */
+int lede_create(const lede_config* cfg, void* weight_arena, size_t weight_bytes, void* kv_pool,
+                size_t kv_bytes, void* workspace, size_t workspace_bytes, lede_ctx** out);
+
+void lede_destroy(lede_ctx* ctx);
+
+/* Text of the last error on this context (never NULL). */
+const char* lede_last_error(const lede_ctx* ctx);
+
+/* Repack one tensor from the caller's device buffer `src` (logical layout
+ * above) into the weight arena (tiled for the kernels).  `layer` is ignored
+ * for non-layer tensors.  `src` may be reused once the stream has passed
+ * this call. */
+int lede_load_tensor(lede_ctx* ctx, int32_t kind, int32_t layer, const void* src, void* stream);
+
+/* Seed the KV page free list with a permutation of 0..n_pages-1 (allocation
+ * pops the front).  Only valid while no page is allocated. */
+int lede_set_free_list(lede_ctx* ctx, const int32_t* order, int32_t n);
+
+/* Options: use_graphs -- replay each step shape as a captured HIP graph;
+ * debug -- keep the fp32 logits of the last draft / verify / prefill head
+ * and the Q-values for lede_debug_read. */
+int lede_set_options(lede_ctx* ctx, int32_t use_graphs, int32_t debug);
+
+/* Append n prompt tokens (host int32, each in [0, vocab)) at positions
+ * seq_len .. seq_len+n-1 through all L layers, writing their K/V; the
+ * argmax of the last row becomes the pending token and is returned in
+ * *next_token (host).  Valid when no draft is outstanding.  Synchronises. */
+int lede_prefill(lede_ctx* ctx, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token);
+
+/* Replace the pending token (teacher forcing / resume).  Synchronous. */
+int lede_set_pending(lede_ctx* ctx, int32_t token, void* stream);
+
+/* Roll the sequence back to new_len <= seq_len positions: frees the pages
+ * wholly past it (pushed to the front of the free list in descending
+ * logical order) and discards any outstanding draft. */
+int lede_truncate(lede_ctx* ctx, int32_t new_len, void* stream);
+
+/* Draft k >= 1 tokens from the pending token by running layers 1..l (Section
+ * 2.2) and the shared final RMSNorm + LM head + argmax, writing each draft's
+ * K/V at layers 1..l.  drafts (host, nullable, [k]) receives the tokens
+ * (then the call synchronises).  Leaves a draft outstanding for
+ * lede_verify.  LEDE_E_STATE if a draft is already outstanding. */
+int lede_draft(lede_ctx* ctx, int32_t l, int32_t k, void* stream, int32_t* drafts);
+
+/* Verify the outstanding drafts (or, with none, take one autoregressive
+ * step): rows [pending, d_1..d_k] at positions seq_len..seq_len+k through
+ * all L layers in one pass, greedy acceptance, commit of d_1..d_a and the
+ * verify token y_a, KV truncation to seq_len+a+1.  Outputs (host): accepted
+ * a, tokens [k+1] (d_1..d_a, y_a), n_emitted = a+1, verify (nullable,
+ * [k+1]) the full model's argmax of every row.  Synchronises. */
+int lede_verify(lede_ctx* ctx, void* stream, int32_t* accepted, int32_t* tokens,
+                int32_t* n_emitted, int32_t* verify);
+
+/* One decoding step of the MDP (Section 3.1): the Q-network observes the
+ * final-normed hidden state of the pending token at the smallest candidate
+ * exit layer and scores the (exit, length) grid; the action is `forced` if
+ * non-NULL (the Q-network still runs and is logged when log_qnet != 0), else
+ * its argmax.  k is clamped to n_remaining - 1 (n_remaining = tokens still
+ * to produce, >= 1); with k_eff = 0 the step is one autoregressive step.
+ * Then draft, verify, accept, truncate; *rec is filled.  Synchronises once
+ * at the end (twice when the Q-network chooses the action). */
+int lede_step(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
+              void* stream, lede_step_record* rec);
+
+/* Committed KV length, pending token and the page table (host copies). */
+int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t* block_table,
+                      int32_t cap, int32_t* n_table);
+
+/* Debug read-back (needs set_options(debug=1)); which = 0: logits of the
+ * last head launch [rows][vocab] fp32; 1: Q-values of the last Q-network
+ * run [E*K]; 2: the Q-network's input state [d] fp32.  *rows receives the
+ * row count.  Synchronises. */
+int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows,
+                    void* stream);
+
+/* ---- single-operation entry points (kernel-level tests and tooling) ----- */
+
+/* Bytes of a tiled weight matrix of N x K (dtype LEDE_DTYPE_*). */
+size_t lede_op_tiled_bytes(int32_t dtype, int32_t N, int32_t K);
+
+/* Repack a logical row-major N x K device matrix into the tiled layout the
+ * linear kernels stream (16-row x 1 KiB tiles, K zero-padded). */
+int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* tiled, void* stream);
+
+/* y[m][n] = sum_k W[n][k] x[m][k] (fp32 accumulate) for m < M <= 16 with a
+ * tiled W (N multiple of 16) and x [M][K] in the model dtype (device).
+ * use_mfma = 0 requires M = 1 (the draft path's vector kernel); 1 uses the
+ * matrix-core kernel of the verify path. */
+int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M,
+                   float* y, int32_t use_mfma, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LEDE_H */

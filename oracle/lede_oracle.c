@@ -288,3 +288,11 @@ void oracle_linear_f32(const float* W, const float* b, int N, int K, const doubl
     y[n] = acc + (b ? (double)b[n] : 0.0);
   }
 }
+
+/* y[t][n] = sum_k W[n][k] x[t][k] for a bf16 (is_bf16) or float32 W [N][K]. */
+void oracle_matvec(const void* W, int is_bf16, int N, int K, const double* x, int T, double* y) {
+  OracleModel M;
+  memset(&M, 0, sizeof M);
+  M.is_bf16 = is_bf16;
+  matvec_rows(&M, W, N, K, x, T, y);
+}

@@ -77,6 +77,7 @@ def _bind(L):
     L.oracle_rope.argtypes = [vp, i, i, d]
     L.oracle_rmsnorm_f64.argtypes = [vp, vp, i, d, vp]
     L.oracle_attend.argtypes = [vp, vp, vp, i, i, vp, vp]
+    L.oracle_matvec.argtypes = [vp, i, i, i, vp, i, vp]
     L.oracle_round_bf16.argtypes = [d]
     L.oracle_round_bf16.restype = d
     return L
@@ -165,6 +166,17 @@ class OracleDecoder:
         h = self.forward([token], pos, l_min)
         _, normed = self.head(h, with_normed=True)
         return normed[0]
+
+
+def matvec(W: np.ndarray, x: np.ndarray, is_bf16: bool) -> np.ndarray:
+    """y[t][n] = sum_k W[n][k] x[t][k] in fp64 (W: uint16 bf16 bits or float32)."""
+    W = np.ascontiguousarray(W)
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    T, K = x.shape
+    N = W.shape[0]
+    y = np.empty((T, N), dtype=np.float64)
+    lib().oracle_matvec(_ptr(W), int(is_bf16), N, K, _ptr(x), T, _ptr(y))
+    return y
 
 
 def argmax_lowest(z: np.ndarray) -> int:
@@ -294,6 +306,8 @@ class SSDState:
         self.c = 0
         self.pending = -1
         self.out: List[int] = []
+        self.last_draft_logits: List[np.ndarray] = []
+        self.last_verify_logits: Optional[np.ndarray] = None
 
     def prefill(self, prompt: Sequence[int]) -> ArgmaxInfo:
         self.pager.ensure(len(prompt))
@@ -322,16 +336,20 @@ class SSDState:
         if not 1 <= l <= L:
             raise ValueError("exit layer out of range")
         self.pager.ensure(self.c + k_eff + 1)
-        drafts, dinfo = [], []
+        drafts, dinfo, dz = [], [], []
         u = self.pending
         for i in range(1, k_eff + 1):
             h = dec.forward([u], self.c + i - 1, l)
-            info = argmax_info(dec.head(h)[0])
+            zi = dec.head(h)[0]
+            info = argmax_info(zi)
             drafts.append(info.token)
             dinfo.append(info)
+            dz.append(zi)
             u = info.token
         h = dec.forward([self.pending] + drafts, self.c, L)
         z = dec.head(h)
+        self.last_draft_logits = dz
+        self.last_verify_logits = z
         vinfo = [argmax_info(z[i]) for i in range(k_eff + 1)]
         verify = [v.token for v in vinfo]
         a = accept_length(drafts, verify)

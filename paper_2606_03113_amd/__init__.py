@@ -1,0 +1,5 @@
+"""MI355X-native batch-1 self-speculative decoding with learned
+(exit layer, draft length) control.  The compute path is liblede.so
+(hand-written gfx950 HIP kernels behind the C ABI in include/lede.h);
+``lede`` is its ctypes binding."""
+from .lede import Engine, LedeError, load, make_config, op_linear  # noqa: F401

@@ -1,0 +1,666 @@
+// gfx950 kernels of the self-speculative decode step.
+//
+// Memory-bound batch-1 decoding: every weight byte is streamed from HBM once
+// per pass.  Weights live in the tiled layout of kernels.h (one coalesced
+// 1 KiB wave load per 16-row x TK tile).  The draft path (one row) uses the
+// vector dot2 instructions; the verify path (k+1 <= 16 rows) uses the
+// 16x16x32 bf16 (or 16x16x4 fp32) matrix-core instructions with the weight
+// tile as the A operand, so one weight read serves every verify row.
+//
+// Determinism: every reduction runs in a fixed order, and the matrix-core
+// result for a row does not depend on the other rows of the call, so a row
+// gives the same bits in a prefill chunk, a verify pass or a one-row
+// autoregressive step.
+#include "kernels.h"
+
+#include <math.h>
+
+namespace lede {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// ---- scalar helpers -------------------------------------------------------
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Round fp32 to bf16, nearest-even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <int DT> struct Elem;
+template <> struct Elem<0> {
+  typedef float T;
+  static __device__ __forceinline__ float load(const void* p, size_t i) { return ((const float*)p)[i]; }
+  static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((float*)p)[i] = v; }
+  static __device__ __forceinline__ float round(float v) { return v; }
+};
+template <> struct Elem<1> {
+  typedef uint16_t T;
+  static __device__ __forceinline__ float load(const void* p, size_t i) { return bf16_to_f32(((const uint16_t*)p)[i]); }
+  static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f32_to_bf16(v); }
+  static __device__ __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
+};
+
+// Orderable 64-bit argmax key: larger value first, then lower index.
+__device__ __forceinline__ uint64_t argmax_key(float v, int idx) {
+  uint32_t u = __float_as_uint(v);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)u << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)idx);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+// Deterministic block sum over 256 threads.
+__device__ __forceinline__ float block_sum256(float v, float* scratch4) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) scratch4[wave] = v;
+  __syncthreads();
+  return scratch4[0] + scratch4[1] + scratch4[2] + scratch4[3];
+}
+
+// 16-byte loads.
+__device__ __forceinline__ uint4 ld16(const void* p) { return *(const uint4*)p; }
+
+// Dot product of one 16-byte weight fragment with one 16-byte x fragment.
+template <int DT> __device__ __forceinline__ float dot16(uint4 w, uint4 x, float acc);
+template <> __device__ __forceinline__ float dot16<1>(uint4 w, uint4 x, float acc) {
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w.x), __builtin_bit_cast(bf16x2, x.x), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w.y), __builtin_bit_cast(bf16x2, x.y), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w.z), __builtin_bit_cast(bf16x2, x.z), acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w.w), __builtin_bit_cast(bf16x2, x.w), acc, false);
+  return acc;
+}
+template <> __device__ __forceinline__ float dot16<0>(uint4 w, uint4 x, float acc) {
+  acc = fmaf(__uint_as_float(w.x), __uint_as_float(x.x), acc);
+  acc = fmaf(__uint_as_float(w.y), __uint_as_float(x.y), acc);
+  acc = fmaf(__uint_as_float(w.z), __uint_as_float(x.z), acc);
+  acc = fmaf(__uint_as_float(w.w), __uint_as_float(x.w), acc);
+  return acc;
+}
+
+// One matrix-core step over a 16 x TK tile: c[n][m] += W[n][k] X[m][k].
+template <int DT> __device__ __forceinline__ f32x4 mfma_tile(uint4 w, uint4 x, f32x4 c);
+template <> __device__ __forceinline__ f32x4 mfma_tile<1>(uint4 w, uint4 x, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), __builtin_bit_cast(bf16x8, x), c, 0, 0, 0);
+}
+template <> __device__ __forceinline__ f32x4 mfma_tile<0>(uint4 w, uint4 x, f32x4 c) {
+  // four K=4 steps; slot j of every lane covers column (l >> 4) * 4 + j
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.x), __uint_as_float(x.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.y), __uint_as_float(x.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.z), __uint_as_float(x.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(w.w), __uint_as_float(x.w), c, 0, 0, 0);
+  return c;
+}
+
+// ---- repack: logical row-major -> tiled -------------------------------------
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_repack(RepackArgs a) {
+  typedef Tile<DT> TL;
+  typedef typename Elem<DT>::T ET;
+  const size_t total = (size_t)a.n_groups * a.KT * 64;
+  for (size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (size_t)gridDim.x * 256) {
+    const int lane = (int)(idx & 63);
+    const size_t rest = idx >> 6;
+    const int t = (int)(rest % a.KT);
+    const int gl = (int)(rest / a.KT);  // group within this call
+    const int r = lane & 15;
+    int row;
+    bool valid = true;
+    switch (a.order) {
+      case ROWS_ROPE: {
+        const int gph = a.hd / 16;
+        const int head = gl / gph, tt = gl % gph;
+        row = head * a.hd + (r < 8 ? 8 * tt + r : a.hd / 2 + 8 * tt + (r - 8));
+        break;
+      }
+      case ROWS_GATE: row = 8 * gl + r; valid = r < 8; break;
+      case ROWS_UP: row = 8 * gl + (r - 8); valid = r >= 8; break;
+      default: row = 16 * gl + r;
+    }
+    if (!valid) continue;  // the other source fills these rows
+    ET vals[TL::EPL];
+    const int k0 = t * TL::TK + (lane >> 4) * TL::EPL;
+#pragma unroll
+    for (int e = 0; e < TL::EPL; ++e) {
+      const int k = k0 + e;
+      vals[e] = (row < a.N && k < a.K) ? ((const ET*)a.src)[(size_t)row * a.K + k] : (ET)0;
+    }
+    uint8_t* dst = (uint8_t*)a.dst + ((size_t)(a.group0 + gl) * a.KT + t) * TILE_BYTES + lane * 16;
+    *(uint4*)dst = *(const uint4*)vals;
+  }
+}
+
+// ---- RMSNorm rows (verify / prefill path and the Q-network's state) ---------
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_norm(NormArgs a) {
+  __shared__ float scratch[4];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  float* h = a.h + (size_t)m * a.ldh;
+  if (m == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
+  const int tok = a.embed ? min((unsigned)a.tok.get(m), (unsigned)(a.vocab - 1)) : 0;
+  if (a.embed) {
+    for (int i = tid; i < a.d; i += 256) h[i] = Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i);
+  }
+  float ss = 0.f;
+  for (int i = tid; i < a.d; i += 256) {
+    const float v = a.embed ? Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i) : h[i];
+    ss += v * v;
+  }
+  ss = block_sum256(ss, scratch);
+  const float inv = rsqrtf(ss / (float)a.d + a.eps);
+  for (int i = tid; i < a.d; i += 256) {
+    const float v = a.embed ? Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i) : h[i];
+    const float y = v * inv * Elem<DT>::load(a.gain, i);
+    if (a.f32_out) ((float*)a.x)[(size_t)m * a.ldx + i] = y;
+    else Elem<DT>::store(a.x, (size_t)m * a.ldx + i, y);
+  }
+}
+
+// ---- linear: y = W x with fused prologue / epilogue --------------------------
+
+// Stage the (single) input row of the vector path in LDS, in the model dtype
+// (fp32 for X_F32), zero-padded to KT * TK elements.
+template <int DT>
+__device__ void stage_x_row(const LinearArgs& a, uint8_t* smem) {
+  typedef Tile<DT> TL;
+  __shared__ float scratch[4];
+  const int tid = threadIdx.x;
+  const int KP = a.KT * TL::TK;
+  if (a.x_mode == X_PLAIN || a.x_mode == X_F32) {
+    for (int i = tid; i < KP; i += 256) {
+      float v = 0.f;
+      if (i < a.K) v = (a.x_mode == X_F32) ? ((const float*)a.x)[i] : Elem<DT>::load(a.x, i);
+      Elem<DT>::store(smem, i, v);
+    }
+  } else {
+    const bool emb = a.x_mode == X_EMBED_NORM;
+    // a token outside the vocabulary can only come from a fault upstream;
+    // clamping keeps the embedding read inside its table
+    const int tok = emb ? (int)min((unsigned)a.tok.get(0), (unsigned)(a.vocab - 1)) : 0;
+    float ss = 0.f;
+    for (int i = tid; i < a.K; i += 256) {
+      const float v = emb ? Elem<DT>::load(a.embed, (size_t)tok * a.K + i) : a.h[i];
+      ss += v * v;
+      if (emb && blockIdx.x == 0) a.h[i] = v;
+    }
+    ss = block_sum256(ss, scratch);
+    const float inv = rsqrtf(ss / (float)a.K + a.eps);
+    for (int i = tid; i < KP; i += 256) {
+      float y = 0.f;
+      if (i < a.K) {
+        const float v = emb ? Elem<DT>::load(a.embed, (size_t)tok * a.K + i) : a.h[i];
+        y = v * inv * Elem<DT>::load(a.gain, i);
+      }
+      Elem<DT>::store(smem, i, y);
+    }
+  }
+  __syncthreads();
+}
+
+template <int DT>
+__device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best) {
+  const int tid = threadIdx.x;
+  const int M = a.M;
+  switch (a.epi) {
+    case EPI_STORE: {
+      const int n = tid >> 4, m = tid & 15;
+      if (m < M) a.out[(size_t)m * a.ldo + g * 16 + n] = ct[n][m];
+      break;
+    }
+    case EPI_BIAS_RELU: {
+      if (tid < 16) {
+        const int row = g * 16 + tid;
+        a.out[row] = fmaxf(ct[tid][0] + a.bias[row], 0.f);
+      }
+      break;
+    }
+    case EPI_RESID: {
+      const int n = tid >> 4, m = tid & 15;
+      if (m < M) a.h[(size_t)m * a.ldh + g * 16 + n] += ct[n][m];
+      break;
+    }
+    case EPI_SWIGLU: {
+      if (tid < 128) {
+        const int r = tid >> 4, m = tid & 15;
+        if (m < M) {
+          const float gt = ct[r][m], up = ct[r + 8][m];
+          const float s = gt / (1.f + __expf(-gt));
+          Elem<DT>::store(a.act, (size_t)m * a.ld_act + 8 * g + r, s * up);
+        }
+      }
+      break;
+    }
+    case EPI_QKV: {
+      const int hd = a.hd, gph = hd / 16;
+      const int qg = a.nq * gph, kg = a.nkv * gph;
+      const int c = *a.seq_len + a.pos_off;
+      if (g < qg + kg) {
+        if (tid < 128) {
+          const int r = tid >> 4, m = tid & 15;
+          if (m < M) {
+            const bool isq = g < qg;
+            const int gl = isq ? g : g - qg;
+            const int head = gl / gph, i = 8 * (gl % gph) + r;
+            const int pos = c + m;
+            const float2 cs = a.rope[(size_t)pos * (hd / 2) + i];
+            const float x0 = ct[r][m], x1 = ct[r + 8][m];
+            const float y0 = x0 * cs.x - x1 * cs.y;
+            const float y1 = x1 * cs.x + x0 * cs.y;
+            if (isq) {
+              float* q = a.q + (size_t)m * a.ldq + head * hd;
+              q[i] = y0;
+              q[i + hd / 2] = y1;
+            } else {
+              const int page = a.block_table[pos >> 6];
+              const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+              Elem<DT>::store(a.kcache, base + i, y0);
+              Elem<DT>::store(a.kcache, base + i + hd / 2, y1);
+            }
+          }
+        }
+      } else {
+        const int n = tid >> 4, m = tid & 15;
+        if (m < M) {
+          const int dim = (g - qg - kg) * 16 + n;
+          const int head = dim / hd, i = dim % hd;
+          const int pos = c + m;
+          const int page = a.block_table[pos >> 6];
+          const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+          Elem<DT>::store(a.vcache, base + i, ct[n][m]);
+        }
+      }
+      break;
+    }
+    case EPI_ARGMAX: {
+      const int n = tid >> 4, m = tid & 15;
+      const int row = g * 16 + n;
+      if (m < M && a.logits) a.logits[(size_t)m * a.ld_logits + row] = ct[n][m];
+      if (tid < 16 && tid < M) {
+        for (int nn = 0; nn < 16; ++nn) {
+          const int rr = g * 16 + nn;
+          if (rr < a.vocab) {
+            const uint64_t key = argmax_key(ct[nn][tid], rr);
+            best = key > best ? key : best;
+          }
+        }
+      }
+      break;
+    }
+  }
+}
+
+template <int DT, bool MFMA>
+__global__ __launch_bounds__(256) void k_linear(LinearArgs a) {
+  typedef Tile<DT> TL;
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ float red[4][16][16];
+  __shared__ float ct[16][17];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+
+  if (blockIdx.x == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
+  if (!MFMA) stage_x_row<DT>(a, smem);
+
+  uint64_t best = 0;
+  const int KT = a.KT;
+  for (int g = blockIdx.x; g < a.n_groups; g += gridDim.x) {
+    const uint8_t* wg = a.w + (size_t)g * KT * TILE_BYTES + lane * 16;
+    if (!MFMA) {
+      const uint8_t* xs = smem + (lane >> 4) * 16;
+      float acc0 = 0.f, acc1 = 0.f;
+      int t = wave;
+      for (; t + 28 < KT; t += 32) {
+        uint4 w[8], x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) w[u] = ld16(wg + (size_t)(t + 4 * u) * TILE_BYTES);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = ld16(xs + (t + 4 * u) * 64);
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          acc0 = dot16<DT>(w[u], x[u], acc0);
+          acc1 = dot16<DT>(w[u + 1], x[u + 1], acc1);
+        }
+      }
+      for (; t < KT; t += 4) acc0 = dot16<DT>(ld16(wg + (size_t)t * TILE_BYTES), ld16(xs + t * 64), acc0);
+      float acc = acc0 + acc1;
+      acc += __shfl_xor(acc, 16);
+      acc += __shfl_xor(acc, 32);
+      if (lane < 16) red[wave][lane][0] = acc;
+    } else {
+      const int m = lane & 15;
+      const bool has = m < a.M;
+      const uint8_t* xr = (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
+      f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+      const uint4 zero = {0u, 0u, 0u, 0u};
+      int t = wave;
+      for (; t + 28 < KT; t += 32) {
+        uint4 w[8], x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) w[u] = ld16(wg + (size_t)(t + 4 * u) * TILE_BYTES);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = has ? ld16(xr + (size_t)(t + 4 * u) * TL::TK * TL::ES) : zero;
+#pragma unroll
+        for (int u = 0; u < 8; u += 2) {
+          c0 = mfma_tile<DT>(w[u], x[u], c0);
+          c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
+        }
+      }
+      for (; t < KT; t += 4) {
+        const uint4 xv = has ? ld16(xr + (size_t)t * TL::TK * TL::ES) : zero;
+        c0 = mfma_tile<DT>(ld16(wg + (size_t)t * TILE_BYTES), xv, c0);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = c0[i] + c1[i];
+    }
+    __syncthreads();
+    {
+      const int n = tid >> 4, m = tid & 15;
+      if (MFMA || m == 0) ct[n][m] = ((red[0][n][m] + red[1][n][m]) + red[2][n][m]) + red[3][n][m];
+    }
+    __syncthreads();
+    epilogue<DT>(a, g, ct, best);
+    __syncthreads();
+  }
+  if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
+    atomicMax((unsigned long long*)&a.keys[tid], (unsigned long long)best);
+}
+
+// ---- attention over the paged KV cache --------------------------------------
+
+// Partial attention of up to 16 query rows (row = (m, query head of the
+// group)) against whole 64-token pages; pages are strided over the blocks of
+// a split.  For every (row, page): running max, sum of exp and the
+// exp-weighted value sum, stored for the combine kernel.
+template <int DT, int HD>
+__global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
+  constexpr int NP = 4, DPP = HD / NP, NPC = DPP / 8;  // score parts, dims per part, 8-pieces
+  constexpr int PV_DG = HD / 8, PV_TG = 256 / PV_DG, TPT = 64 / PV_TG;
+  __shared__ float qs[16][HD];
+  __shared__ float ss[16][64];
+  __shared__ float st_m[16], st_l[16];
+  __shared__ float red[4][16][HD];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int G = a.nq / a.nkv;
+  const int R = a.M * G;
+  const int n_rs = (R + a.rows_per_block - 1) / a.rows_per_block;
+  const int kvh = blockIdx.x / n_rs, rs = blockIdx.x % n_rs;
+  const int r0 = rs * a.rows_per_block;
+  const int nr = min(a.rows_per_block, R - r0);
+  const int pos0 = *a.seq_len + a.pos_off;
+  const int pmax = pos0 + a.M - 1;
+  const int n_chunks = pmax / 64 + 1;
+  const float scale = rsqrtf((float)HD);
+
+  for (int idx = tid; idx < nr * HD; idx += 256) {
+    const int r = idx / HD, i = idx % HD;
+    const int rr = r0 + r, m = rr / G, head = kvh * G + rr % G;
+    qs[r][i] = a.q[(size_t)m * a.ldq + head * HD + i] * scale;
+  }
+  __syncthreads();
+
+  for (int j = blockIdx.y; j < n_chunks; j += a.n_split) {
+    const int page = a.block_table[j];
+    const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
+    const int tok0 = j * 64;
+    const int nvalid = min(64, pmax - tok0 + 1);
+    {  // scores
+      const int t = tid >> 2, p = tid & 3;
+      float kf[DPP];
+      if (t < nvalid) {
+#pragma unroll
+        for (int c = 0; c < NPC; ++c)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kf[8 * c + e] = Elem<DT>::load(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c + e);
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPP; ++e) kf[e] = 0.f;
+      }
+      for (int r = 0; r < nr; ++r) {
+        float s = 0.f;
+#pragma unroll
+        for (int c = 0; c < NPC; ++c)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) s = fmaf(qs[r][p * 8 + 32 * c + e], kf[8 * c + e], s);
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        const int m = (r0 + r) / G;
+        if (p == 0) ss[r][t] = (tok0 + t <= pos0 + m) ? s : -INFINITY;
+      }
+    }
+    __syncthreads();
+    for (int r = wave; r < nr; r += 4) {  // softmax statistics, one lane per token
+      const float v = ss[r][lane];
+      const float mx = wave_max(v);
+      const float e = (v == -INFINITY) ? 0.f : __expf(v - mx);
+      const float l = wave_sum(e);
+      ss[r][lane] = e;
+      if (lane == 0) {
+        st_m[r] = mx;
+        st_l[r] = l;
+      }
+    }
+    __syncthreads();
+    {  // exp-weighted values
+      const int dg = tid % PV_DG, tg = tid / PV_DG;
+      float vf[TPT][8];
+#pragma unroll
+      for (int u = 0; u < TPT; ++u) {
+        const int t = tg + PV_TG * u;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          vf[u][e] = (t < nvalid) ? Elem<DT>::load(a.vcache, base + (size_t)t * HD + dg * 8 + e) : 0.f;
+      }
+      for (int r = 0; r < nr; ++r) {
+        float o[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = 0.f;
+#pragma unroll
+        for (int u = 0; u < TPT; ++u) {
+          const float w = ss[r][tg + PV_TG * u];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = fmaf(w, vf[u][e], o[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          for (int off = PV_DG; off < 64; off <<= 1) o[e] += __shfl_xor(o[e], off);
+        if (lane < PV_DG) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) red[wave][r][dg * 8 + e] = o[e];
+        }
+      }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < nr * HD; idx += 256) {
+      const int r = idx / HD, i = idx % HD;
+      const int rr = r0 + r, m = rr / G, head = kvh * G + rr % G;
+      float* p = a.part + (((size_t)m * a.nq + head) * a.max_chunks + j) * (HD + 2);
+      p[2 + i] = ((red[0][r][i] + red[1][r][i]) + red[2][r][i]) + red[3][r][i];
+      if (i == 0) {
+        p[0] = st_m[r];
+        p[1] = st_l[r];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Combine the per-page partials of every (row, head) in page order.
+template <int DT, int HD>
+__global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
+  const int m = blockIdx.x / a.nq, head = blockIdx.x % a.nq, i = threadIdx.x;
+  const int pos = *a.seq_len + a.pos_off + m;
+  const int nc = pos / 64 + 1;
+  const float* p = a.part + ((size_t)m * a.nq + head) * a.max_chunks * (HD + 2);
+  float mx = -INFINITY, l = 0.f, acc = 0.f;
+  for (int j = 0; j < nc; ++j, p += HD + 2) {
+    const float pm = p[0], pl = p[1], pa = p[2 + i];
+    const float nm = fmaxf(mx, pm);
+    const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
+    const float sn = __expf(pm - nm);
+    l = l * so + pl * sn;
+    acc = acc * so + pa * sn;
+    mx = nm;
+  }
+  Elem<DT>::store(a.out, (size_t)m * a.ldo + head * HD + i, acc / l);
+}
+
+// ---- Q-network output layer + argmax ----------------------------------------
+
+__global__ __launch_bounds__(256) void k_qnet_out(QnetOutArgs a) {
+  __shared__ unsigned long long best[256];
+  const int tid = threadIdx.x;
+  uint64_t b = 0;
+  for (int j = tid; j < a.A; j += 256) {
+    float s = 0.f;
+    for (int i = 0; i < a.H; ++i) s = fmaf(a.w2[(size_t)j * a.H + i], a.hid[i], s);
+    s += a.b2[j];
+    a.qv[j] = s;
+    const uint64_t key = argmax_key(s, j);
+    b = key > b ? key : b;
+  }
+  best[tid] = b;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) best[tid] = best[tid + o] > best[tid] ? best[tid + o] : best[tid];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const int idx = (int)(0xFFFFFFFFu - (uint32_t)(best[0] & 0xFFFFFFFFull));
+    a.action[0] = idx;
+    a.action[1] = __float_as_int(a.qv[idx]);
+  }
+}
+
+// ---- greedy acceptance scan + commit + KV truncation --------------------------
+
+__global__ void k_accept(AcceptArgs a) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  TokenSrc dk = {nullptr, a.dkeys}, vk = {nullptr, a.vkeys};
+  const int k = a.k;
+  int acc = 0;
+  while (acc < k && dk.get(acc + 1) == vk.get(acc)) ++acc;
+  const int c = *a.seq_len;
+  const int c_new = c + acc + 1;
+  const int y = vk.get(acc);
+  for (int i = 0; i < acc; ++i) a.record[4 + i] = dk.get(i + 1);
+  a.record[4 + acc] = y;
+  for (int i = 0; i < k; ++i) a.record[24 + i] = dk.get(i + 1);
+  a.record[0] = acc;
+  a.record[1] = acc + 1;
+  a.record[2] = c_new;
+  a.record[3] = y;
+  *a.seq_len = c_new;
+  a.pending_out[0] = (uint64_t)(0xFFFFFFFFu - (uint32_t)y);
+  // pages wholly past the committed length go back to the pool
+  const int keep = (c_new + 63) / 64, used = (c + k + 1 + 63) / 64;
+  for (int j = keep; j < used; ++j) a.block_table[j] = -1;
+}
+
+__global__ void k_fill_u64(uint64_t* p, uint64_t v, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void k_set_token(uint64_t* keys, int idx, int token) {
+  if (threadIdx.x == 0) keys[idx] = (uint64_t)(0xFFFFFFFFu - (uint32_t)token);
+}
+
+// ---- launchers ----------------------------------------------------------------
+
+hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
+  const size_t total = (size_t)a.n_groups * a.KT * 64;
+  const int grid = (int)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
+  if (dtype == 1) hipLaunchKernelGGL(k_repack<1>, dim3(grid), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_repack<0>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s) {
+  if (dtype == 1) hipLaunchKernelGGL(k_norm<1>, dim3(a.M), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_norm<0>, dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
+  (void)M;
+  if (mfma) return 0;
+  const int tk = tile_k(dtype);
+  const int kp = ((K + tk - 1) / tk) * tk;
+  return (size_t)kp * (dtype == 1 ? 2 : 4);
+}
+
+hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s) {
+  const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
+  if (dtype == 1) {
+    if (mfma) hipLaunchKernelGGL((k_linear<1, true>), dim3(grid), dim3(256), lds, s, a);
+    else hipLaunchKernelGGL((k_linear<1, false>), dim3(grid), dim3(256), lds, s, a);
+  } else {
+    if (mfma) hipLaunchKernelGGL((k_linear<0, true>), dim3(grid), dim3(256), lds, s, a);
+    else hipLaunchKernelGGL((k_linear<0, false>), dim3(grid), dim3(256), lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
+  const int G = a.nq / a.nkv;
+  const int n_rs = (a.M * G + a.rows_per_block - 1) / a.rows_per_block;
+  dim3 grid(a.nkv * n_rs, a.n_split);
+  const int combine_grid = a.M * a.nq;
+  if (dtype == 1) {
+    if (a.hd == 128) {
+      hipLaunchKernelGGL((k_attn_partial<1, 128>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<1, 128>), dim3(combine_grid), dim3(128), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_attn_partial<1, 64>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<1, 64>), dim3(combine_grid), dim3(64), 0, s, a);
+    }
+  } else {
+    if (a.hd == 128) {
+      hipLaunchKernelGGL((k_attn_partial<0, 128>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<0, 128>), dim3(combine_grid), dim3(128), 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_attn_partial<0, 64>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<0, 64>), dim3(combine_grid), dim3(64), 0, s, a);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_qnet_out, dim3(1), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s) {
+  hipLaunchKernelGGL(k_fill_u64, dim3((n + 255) / 256), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s) {
+  hipLaunchKernelGGL(k_set_token, dim3(1), dim3(64), 0, s, keys, idx, token);
+  return hipGetLastError();
+}
+
+}  // namespace lede

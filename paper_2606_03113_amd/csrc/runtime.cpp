@@ -1,0 +1,808 @@
+// liblede host runtime: context, KV page allocator, orchestration of the
+// draft / verify passes, and the C ABI declared in include/lede.h.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/lede.h"
+#include "kernels.h"
+
+using namespace lede;
+
+namespace {
+
+constexpr int PAGE = 64;
+constexpr int MROWS = 16;   // rows of one verify / prefill pass
+constexpr int RECORD_INTS = 64;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  // element sizes and padded dims
+  int dt, es, L, d, nq, nkv, hd, F, V, qd, kvd, Fp, H, A, max_ctx, n_pages, max_pages_seq, max_chunks, k_max;
+  // weight arena offsets
+  struct LayerOff { size_t attn_norm, wqkv, wo, ffn_norm, wgu, wd; };
+  std::vector<LayerOff> lay;
+  size_t embed, final_norm, head, qw1, qb1, qw2, qb2, wbytes;
+  // workspace offsets
+  size_t h, xn, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
+      record, rope, wsbytes;
+  size_t kvbytes, kv_half;
+};
+
+const char* check_config(const lede_config* c) {
+  if (!c) return "null config";
+  if (c->dtype != LEDE_DTYPE_F32 && c->dtype != LEDE_DTYPE_BF16) return "dtype must be f32 or bf16";
+  if (c->n_layers < 1 || c->d_model < 32 || c->n_heads < 1 || c->n_kv_heads < 1 || c->vocab < 16)
+    return "bad model dims";
+  if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
+  if (c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
+  if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32) return "d_model and n_heads*head_dim must be multiples of 32";
+  if (c->ffn_dim % 8 || c->ffn_dim < 8) return "ffn_dim must be a multiple of 8";
+  if (c->vocab % 16) return "vocab must be a multiple of 16";
+  if (c->page_size != PAGE) return "page_size must be 64";
+  if (c->max_ctx < 1 || c->n_pages < 1) return "bad KV geometry";
+  if (c->k_max < 0 || c->k_max > 15) return "k_max must be in 0..15";
+  if (c->qnet_hidden < 0 || c->qnet_hidden % 16) return "qnet_hidden must be a multiple of 16";
+  if (c->qnet_hidden > 0) {
+    if (c->n_exits < 1 || c->n_exits > 64 || c->n_lengths < 1 || c->n_lengths > 16) return "bad action grid";
+    for (int i = 0; i < c->n_exits; ++i)
+      if (c->exits[i] < 1 || c->exits[i] > c->n_layers || (i && c->exits[i] <= c->exits[i - 1]))
+        return "exits must be ascending in 1..n_layers";
+    for (int i = 0; i < c->n_lengths; ++i)
+      if (c->lengths[i] < 1 || c->lengths[i] > 16) return "lengths must be in 1..16";
+  }
+  return nullptr;
+}
+
+Layout make_layout(const lede_config* c) {
+  Layout o{};
+  o.dt = c->dtype;
+  o.es = c->dtype == LEDE_DTYPE_BF16 ? 2 : 4;
+  o.L = c->n_layers; o.d = c->d_model; o.nq = c->n_heads; o.nkv = c->n_kv_heads; o.hd = c->head_dim;
+  o.F = c->ffn_dim; o.V = c->vocab; o.qd = o.nq * o.hd; o.kvd = o.nkv * o.hd;
+  const int tk = tile_k(o.dt);
+  o.Fp = (o.F + tk - 1) / tk * tk;
+  o.H = c->qnet_hidden; o.A = c->qnet_hidden ? c->n_exits * c->n_lengths : 0;
+  o.max_ctx = c->max_ctx; o.n_pages = c->n_pages; o.k_max = c->k_max;
+  o.max_pages_seq = (o.max_ctx + PAGE - 1) / PAGE;
+  o.max_chunks = o.max_pages_seq;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t r = off; off += align256(bytes); return r; };
+  o.lay.resize(o.L);
+  for (int l = 0; l < o.L; ++l) {
+    auto& x = o.lay[l];
+    x.attn_norm = take((size_t)o.d * o.es);
+    x.wqkv = take(tiled_bytes(o.dt, o.qd + 2 * o.kvd, o.d));
+    x.wo = take(tiled_bytes(o.dt, o.d, o.qd));
+    x.ffn_norm = take((size_t)o.d * o.es);
+    x.wgu = take(tiled_bytes(o.dt, 2 * o.F, o.d));
+    x.wd = take(tiled_bytes(o.dt, o.d, o.F));
+  }
+  o.embed = take((size_t)o.V * o.d * o.es);
+  o.final_norm = take((size_t)o.d * o.es);
+  o.head = take(tiled_bytes(o.dt, o.V, o.d));
+  o.qw1 = take(o.H ? tiled_bytes(0, o.H, o.d) : 0);
+  o.qb1 = take((size_t)o.H * 4);
+  o.qw2 = take((size_t)o.A * o.H * 4);
+  o.qb2 = take((size_t)o.A * 4);
+  o.wbytes = off;
+
+  off = 0;
+  o.h = take((size_t)MROWS * o.d * 4);
+  o.xn = take((size_t)MROWS * o.d * o.es);
+  o.q = take((size_t)MROWS * o.qd * 4);
+  o.attn_out = take((size_t)MROWS * o.qd * o.es);
+  o.act = take((size_t)MROWS * o.Fp * o.es);
+  o.part = take((size_t)MROWS * o.nq * o.max_chunks * (o.hd + 2) * 4);
+  o.logits = take((size_t)2 * MROWS * o.V * 4);
+  o.dkeys = take(32 * 8);
+  o.vkeys = take(MROWS * 8);
+  o.qs = take((size_t)o.d * 4);
+  o.qhid = take((size_t)(o.H ? o.H : 1) * 4);
+  o.qv = take((size_t)(o.A ? o.A : 1) * 4);
+  o.qaction = take(16 * 4);
+  o.seq_len = take(4);
+  o.btab = take((size_t)o.max_pages_seq * 4);
+  o.prompt = take((size_t)o.max_ctx * 4);
+  o.record = take(RECORD_INTS * 4);
+  o.rope = take((size_t)o.max_ctx * (o.hd / 2) * 8);
+  o.wsbytes = off;
+
+  o.kv_half = align256((size_t)o.L * o.n_pages * o.nkv * PAGE * o.hd * o.es);
+  o.kvbytes = 2 * o.kv_half;
+  return o;
+}
+
+}  // namespace
+
+struct lede_ctx {
+  lede_config cfg;
+  Layout lo;
+  uint8_t *w, *kv, *ws;
+  int dev;
+  // host mirror of the decoding state
+  int32_t seq_len = 0;
+  int32_t pending = -1;
+  int drafted_k = -1;  // -1: no draft outstanding
+  int drafted_l = 0;
+  std::deque<int32_t> free_list;
+  std::vector<int32_t> table;
+  int32_t* table_h = nullptr;   // pinned mirror uploaded to the device table
+  int32_t* record_h = nullptr;  // pinned read-back of the step record
+  uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
+  int use_graphs = 0, debug = 0;
+  int last_rows = 0, last_draft_rows = 0;
+  std::string err;
+
+  // device pointers
+  template <typename T> T* W(size_t off) const { return (T*)(w + off); }
+  template <typename T> T* S(size_t off) const { return (T*)(ws + off); }
+};
+
+namespace {
+
+int fail(lede_ctx* c, int code, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return code;
+}
+
+#define HIP_CHECK(ctx, expr)                                                               \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail(ctx, LEDE_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+hipStream_t S_(void* s) { return (hipStream_t)s; }
+
+// ---- page allocator (host) ------------------------------------------------------
+
+int ensure_pages(lede_ctx* c, int n_positions) {
+  if (n_positions > c->lo.max_ctx) return fail(c, LEDE_E_CTX_OVERFLOW, "position %d exceeds max_ctx %d", n_positions, c->lo.max_ctx);
+  const int need = (n_positions + PAGE - 1) / PAGE;
+  if (need - (int)c->table.size() > (int)c->free_list.size())
+    return fail(c, LEDE_E_KV_FULL, "KV pool exhausted (%d pages needed, %zu free)", need, c->free_list.size());
+  while ((int)c->table.size() < need) {
+    c->table.push_back(c->free_list.front());
+    c->free_list.pop_front();
+  }
+  return LEDE_OK;
+}
+
+void truncate_pages(lede_ctx* c, int new_len) {
+  const int keep = (new_len + PAGE - 1) / PAGE;
+  for (int j = (int)c->table.size() - 1; j >= keep; --j) c->free_list.push_front(c->table[j]);
+  if ((int)c->table.size() > keep) c->table.resize(keep);
+}
+
+int upload_table(lede_ctx* c, hipStream_t s) {
+  const int n = c->lo.max_pages_seq;
+  for (int j = 0; j < n; ++j) c->table_h[j] = j < (int)c->table.size() ? c->table[j] : -1;
+  HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.btab), c->table_h, n * 4, hipMemcpyHostToDevice, s));
+  return LEDE_OK;
+}
+
+int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
+  c->record_h[RECORD_INTS - 1] = v;
+  HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.seq_len), &c->record_h[RECORD_INTS - 1], 4, hipMemcpyHostToDevice, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  return LEDE_OK;
+}
+
+// ---- pass orchestration -----------------------------------------------------------
+
+int linear_grid(int n_groups, int epi) {
+  const int cap = epi == EPI_ARGMAX ? 1024 : 4096;
+  return std::min(n_groups, cap);
+}
+
+LinearArgs base_linear(const lede_ctx* c) {
+  LinearArgs a{};
+  a.M = 1;
+  a.eps = c->cfg.rms_eps;
+  a.h = c->S<float>(c->lo.h);
+  a.ldh = c->lo.d;
+  return a;
+}
+
+// Run rows [0, M) at positions seq_len + pos_off + m through layers
+// [l_begin, l_end).  Vector kernels for one row (draft path), matrix-core
+// kernels otherwise.  qnet_after: run the Q-network after this many layers
+// (0 = never).
+int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_begin, int l_end, int qnet_after,
+               uint64_t* zero_slot, hipStream_t s) {
+  const Layout& o = c->lo;
+  const int dt = o.dt;
+  for (int j = l_begin; j < l_end; ++j) {
+    const auto& lw = o.lay[j];
+    const bool first = j == 0;
+    // attention block: [norm] + QKV (rotary, KV append)
+    LinearArgs qa = base_linear(c);
+    qa.M = M;
+    qa.w = c->W<uint8_t>(lw.wqkv);
+    qa.n_groups = (o.qd + 2 * o.kvd) / 16;
+    qa.KT = k_tiles(dt, o.d);
+    qa.K = o.d;
+    qa.epi = EPI_QKV;
+    qa.q = c->S<float>(o.q); qa.ldq = o.qd;
+    qa.kcache = c->kv; qa.vcache = c->kv + o.kv_half;
+    qa.layer = j; qa.n_pages = o.n_pages; qa.nq = o.nq; qa.nkv = o.nkv; qa.hd = o.hd;
+    qa.block_table = c->S<int32_t>(o.btab); qa.seq_len = c->S<int32_t>(o.seq_len); qa.pos_off = pos_off;
+    qa.rope = c->S<float2>(o.rope);
+    if (vec) {
+      qa.x_mode = first ? X_EMBED_NORM : X_NORM;
+      qa.gain = c->W<void>(lw.attn_norm);
+      qa.embed = c->W<void>(o.embed);
+      qa.tok = tok;
+      qa.vocab = o.V;
+      if (first && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = 1; }
+    } else {
+      NormArgs na{};
+      na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
+      na.h = c->S<float>(o.h); na.gain = c->W<void>(lw.attn_norm); na.eps = c->cfg.rms_eps;
+      na.embed = first; na.embed_w = c->W<void>(o.embed); na.tok = tok; na.vocab = o.V;
+      na.x = c->S<void>(o.xn);
+      if (first && zero_slot) { na.zero_keys = zero_slot; na.n_zero_keys = M; }
+      HIP_CHECK(c, launch_norm(dt, na, s));
+      qa.x_mode = X_PLAIN; qa.x = c->S<void>(o.xn); qa.ldx = o.d;
+    }
+    HIP_CHECK(c, launch_linear(dt, !vec, qa, linear_grid(qa.n_groups, qa.epi), s));
+
+    AttnArgs at{};
+    at.q = c->S<float>(o.q); at.ldq = o.qd;
+    at.kcache = c->kv; at.vcache = c->kv + o.kv_half;
+    at.layer = j; at.n_pages = o.n_pages; at.nq = o.nq; at.nkv = o.nkv; at.hd = o.hd; at.M = M;
+    at.block_table = c->S<int32_t>(o.btab); at.seq_len = c->S<int32_t>(o.seq_len); at.pos_off = pos_off;
+    const int G = o.nq / o.nkv;
+    at.rows_per_block = std::min(16, M * G);
+    const int n_rs = (M * G + at.rows_per_block - 1) / at.rows_per_block;
+    at.n_split = std::max(1, std::min(o.max_chunks, (512 + o.nkv * n_rs - 1) / (o.nkv * n_rs)));
+    at.max_chunks = o.max_chunks;
+    at.part = c->S<float>(o.part);
+    at.out = c->S<void>(o.attn_out); at.ldo = o.qd;
+    HIP_CHECK(c, launch_attention(dt, at, s));
+
+    LinearArgs oa = base_linear(c);
+    oa.M = M;
+    oa.w = c->W<uint8_t>(lw.wo);
+    oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
+    oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
+    oa.epi = EPI_RESID;
+    HIP_CHECK(c, launch_linear(dt, !vec, oa, linear_grid(oa.n_groups, oa.epi), s));
+
+    // feed-forward block
+    LinearArgs ga = base_linear(c);
+    ga.M = M;
+    ga.w = c->W<uint8_t>(lw.wgu);
+    ga.n_groups = 2 * o.F / 16; ga.KT = k_tiles(dt, o.d); ga.K = o.d;
+    ga.epi = EPI_SWIGLU; ga.act = c->S<void>(o.act); ga.ld_act = o.Fp;
+    if (vec) {
+      ga.x_mode = X_NORM; ga.gain = c->W<void>(lw.ffn_norm);
+    } else {
+      NormArgs na{};
+      na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
+      na.h = c->S<float>(o.h); na.gain = c->W<void>(lw.ffn_norm); na.eps = c->cfg.rms_eps;
+      na.x = c->S<void>(o.xn);
+      HIP_CHECK(c, launch_norm(dt, na, s));
+      ga.x_mode = X_PLAIN; ga.x = c->S<void>(o.xn); ga.ldx = o.d;
+    }
+    HIP_CHECK(c, launch_linear(dt, !vec, ga, linear_grid(ga.n_groups, ga.epi), s));
+
+    LinearArgs da = base_linear(c);
+    da.M = M;
+    da.w = c->W<uint8_t>(lw.wd);
+    da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
+    da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
+    da.epi = EPI_RESID;
+    HIP_CHECK(c, launch_linear(dt, !vec, da, linear_grid(da.n_groups, da.epi), s));
+
+    if (qnet_after == j + 1 && o.H > 0) {
+      NormArgs na{};
+      na.M = 1; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
+      na.h = c->S<float>(o.h); na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
+      na.x = c->S<void>(o.qs); na.f32_out = 1;
+      HIP_CHECK(c, launch_norm(dt, na, s));
+      LinearArgs la = base_linear(c);
+      la.w = c->W<uint8_t>(o.qw1);
+      la.n_groups = o.H / 16; la.KT = k_tiles(0, o.d); la.K = o.d;
+      la.x_mode = X_F32; la.x = c->S<void>(o.qs);
+      la.epi = EPI_BIAS_RELU; la.out = c->S<float>(o.qhid); la.bias = c->W<float>(o.qb1);
+      HIP_CHECK(c, launch_linear(0, false, la, la.n_groups, s));
+      QnetOutArgs qo{};
+      qo.hid = c->S<float>(o.qhid); qo.H = o.H;
+      qo.w2 = c->W<float>(o.qw2); qo.b2 = c->W<float>(o.qb2); qo.A = o.A;
+      qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.qaction);
+      HIP_CHECK(c, launch_qnet_out(qo, s));
+    }
+  }
+  return LEDE_OK;
+}
+
+// Shared final RMSNorm + LM head + argmax for rows [0, M) into keys[0..M).
+int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s) {
+  const Layout& o = c->lo;
+  LinearArgs ha = base_linear(c);
+  ha.M = M;
+  ha.w = c->W<uint8_t>(o.head);
+  ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
+  ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
+  ha.logits = logits; ha.ld_logits = o.V;
+  if (vec) {
+    ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
+  } else {
+    NormArgs na{};
+    na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
+    na.h = c->S<float>(o.h); na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
+    na.x = c->S<void>(o.xn);
+    HIP_CHECK(c, launch_norm(o.dt, na, s));
+    ha.x_mode = X_PLAIN; ha.x = c->S<void>(o.xn); ha.ldx = o.d;
+  }
+  HIP_CHECK(c, launch_linear(o.dt, !vec, ha, linear_grid(ha.n_groups, ha.epi), s));
+  return LEDE_OK;
+}
+
+float* draft_logits(lede_ctx* c, int i) {
+  return c->debug ? c->S<float>(c->lo.logits) + (size_t)(MROWS + i) * c->lo.V : nullptr;
+}
+float* verify_logits(lede_ctx* c) { return c->debug ? c->S<float>(c->lo.logits) : nullptr; }
+
+// Draft passes i = i0..k (1-based): token i-1 -> layers [0, l) -> head -> key i.
+// qnet_after applies to pass 1 only.
+int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_begin, hipStream_t s) {
+  uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
+  for (int i = i0; i <= k; ++i) {
+    TokenSrc tok{nullptr, dk + (i - 1)};
+    const int begin = i == 1 ? pass1_begin : 0;
+    int rc = run_layers(c, 1, true, tok, i - 1, begin, l, i == 1 ? qnet_after : 0, dk + i, s);
+    if (rc) return rc;
+    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1), s);
+    if (rc) return rc;
+  }
+  c->last_draft_rows = k;
+  return LEDE_OK;
+}
+
+int launch_verify(lede_ctx* c, int k, hipStream_t s) {
+  uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
+  uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
+  TokenSrc tok{nullptr, dk};
+  int rc = run_layers(c, k + 1, false, tok, 0, 0, c->lo.L, 0, vk, s);
+  if (rc) return rc;
+  rc = run_head(c, k + 1, false, vk, verify_logits(c), s);
+  if (rc) return rc;
+  AcceptArgs aa{};
+  aa.dkeys = dk; aa.vkeys = vk; aa.k = k;
+  aa.seq_len = c->S<int32_t>(c->lo.seq_len);
+  aa.block_table = c->S<int32_t>(c->lo.btab);
+  aa.pending_out = dk;
+  aa.record = c->S<int32_t>(c->lo.record);
+  HIP_CHECK(c, launch_accept(aa, s));
+  c->last_rows = k + 1;
+  return LEDE_OK;
+}
+
+int read_record(lede_ctx* c, hipStream_t s) {
+  HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 48 * 4, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  return LEDE_OK;
+}
+
+// Apply a finished verify (record read back) to the host mirror.
+void commit_host(lede_ctx* c) {
+  c->seq_len = c->record_h[2];
+  c->pending = c->record_h[3];
+  truncate_pages(c, c->seq_len);
+  c->drafted_k = -1;
+}
+
+}  // namespace
+
+// ---- C ABI -------------------------------------------------------------------------
+
+extern "C" {
+
+int lede_region_bytes(const lede_config* cfg, size_t* wb, size_t* kvb, size_t* wsb) {
+  if (const char* why = check_config(cfg)) { (void)why; return cfg ? LEDE_E_UNSUPPORTED : LEDE_E_ARG; }
+  Layout o = make_layout(cfg);
+  if (wb) *wb = o.wbytes;
+  if (kvb) *kvb = o.kvbytes;
+  if (wsb) *wsb = o.wsbytes;
+  return LEDE_OK;
+}
+
+const char* lede_last_error(const lede_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, size_t kvbytes, void* ws,
+                size_t wsbytes, lede_ctx** out) {
+  if (!out) return LEDE_E_ARG;
+  *out = nullptr;
+  if (!cfg || !warena || !kv || !ws) return LEDE_E_ARG;
+  if (check_config(cfg)) return LEDE_E_UNSUPPORTED;
+  Layout o = make_layout(cfg);
+  if (wbytes < o.wbytes || kvbytes < o.kvbytes || wsbytes < o.wsbytes) return LEDE_E_ARG;
+  if (((uintptr_t)warena | (uintptr_t)kv | (uintptr_t)ws) & 255) return LEDE_E_ARG;
+  lede_ctx* c = new lede_ctx();
+  c->cfg = *cfg;
+  c->lo = o;
+  c->w = (uint8_t*)warena;
+  c->kv = (uint8_t*)kv;
+  c->ws = (uint8_t*)ws;
+  (void)hipGetDevice(&c->dev);
+  for (int i = 0; i < o.n_pages; ++i) c->free_list.push_back(i);
+  if (hipHostMalloc((void**)&c->table_h, (size_t)o.max_pages_seq * 4 + 256, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->record_h, RECORD_INTS * 4, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->keys_h, 32 * 8, 0) != hipSuccess) {
+    lede_destroy(c);
+    return LEDE_E_HIP;
+  }
+  // zero the workspace (padding columns of activations must be finite)
+  if (hipMemset(ws, 0, o.wsbytes) != hipSuccess) { lede_destroy(c); return LEDE_E_HIP; }
+  // rotary table: angle pos * base^(-2i/hd) in fp64, stored as fp32 (cos, sin)
+  std::vector<float> rope((size_t)o.max_ctx * o.hd);
+  for (int p = 0; p < o.max_ctx; ++p)
+    for (int i = 0; i < o.hd / 2; ++i) {
+      const double ang = (double)p * std::pow((double)cfg->rope_base, -2.0 * i / o.hd);
+      rope[((size_t)p * (o.hd / 2) + i) * 2] = (float)std::cos(ang);
+      rope[((size_t)p * (o.hd / 2) + i) * 2 + 1] = (float)std::sin(ang);
+    }
+  if (hipMemcpy(c->S<void>(o.rope), rope.data(), rope.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    lede_destroy(c);
+    return LEDE_E_HIP;
+  }
+  std::vector<int32_t> bt(o.max_pages_seq, -1);
+  if (hipMemcpy(c->S<void>(o.btab), bt.data(), bt.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    lede_destroy(c);
+    return LEDE_E_HIP;
+  }
+  *out = c;
+  return LEDE_OK;
+}
+
+void lede_destroy(lede_ctx* c) {
+  if (!c) return;
+  if (c->table_h) (void)hipHostFree(c->table_h);
+  if (c->record_h) (void)hipHostFree(c->record_h);
+  if (c->keys_h) (void)hipHostFree(c->keys_h);
+  delete c;
+}
+
+int lede_load_tensor(lede_ctx* c, int32_t kind, int32_t layer, const void* src, void* stream) {
+  if (!c || !src) return fail(c, LEDE_E_ARG, "null argument");
+  const Layout& o = c->lo;
+  hipStream_t s = S_(stream);
+  const bool per_layer = kind >= LEDE_T_ATTN_NORM && kind <= LEDE_T_WD;
+  if (per_layer && (layer < 0 || layer >= o.L)) return fail(c, LEDE_E_ARG, "layer %d out of range", layer);
+  auto copy = [&](size_t off, size_t bytes) -> int {
+    HIP_CHECK(c, hipMemcpyAsync(c->w + off, src, bytes, hipMemcpyDeviceToDevice, s));
+    return LEDE_OK;
+  };
+  auto repack = [&](size_t off, int N, int K, int group0, int n_groups, int order, int dt) -> int {
+    RepackArgs ra{};
+    ra.src = src; ra.N = N; ra.K = K; ra.dst = c->w + off; ra.KT = k_tiles(dt, K);
+    ra.group0 = group0; ra.n_groups = n_groups; ra.order = order; ra.hd = o.hd;
+    HIP_CHECK(c, launch_repack(dt, ra, s));
+    return LEDE_OK;
+  };
+  const auto* lw = per_layer ? &o.lay[layer] : nullptr;
+  const size_t ed = (size_t)o.d * o.es;
+  switch (kind) {
+    case LEDE_T_EMBED: return copy(o.embed, (size_t)o.V * ed);
+    case LEDE_T_FINAL_NORM: return copy(o.final_norm, ed);
+    case LEDE_T_HEAD: return repack(o.head, o.V, o.d, 0, o.V / 16, ROWS_PLAIN, o.dt);
+    case LEDE_T_ATTN_NORM: return copy(lw->attn_norm, ed);
+    case LEDE_T_FFN_NORM: return copy(lw->ffn_norm, ed);
+    case LEDE_T_WQ: return repack(lw->wqkv, o.qd, o.d, 0, o.qd / 16, ROWS_ROPE, o.dt);
+    case LEDE_T_WK: return repack(lw->wqkv, o.kvd, o.d, o.qd / 16, o.kvd / 16, ROWS_ROPE, o.dt);
+    case LEDE_T_WV: return repack(lw->wqkv, o.kvd, o.d, (o.qd + o.kvd) / 16, o.kvd / 16, ROWS_PLAIN, o.dt);
+    case LEDE_T_WO: return repack(lw->wo, o.d, o.qd, 0, o.d / 16, ROWS_PLAIN, o.dt);
+    case LEDE_T_WG: return repack(lw->wgu, o.F, o.d, 0, o.F / 8, ROWS_GATE, o.dt);
+    case LEDE_T_WU: return repack(lw->wgu, o.F, o.d, 0, o.F / 8, ROWS_UP, o.dt);
+    case LEDE_T_WD: return repack(lw->wd, o.d, o.F, 0, o.d / 16, ROWS_PLAIN, o.dt);
+    case LEDE_T_QNET_W1:
+      if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network");
+      return repack(o.qw1, o.H, o.d, 0, o.H / 16, ROWS_PLAIN, 0);
+    case LEDE_T_QNET_B1: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qb1, (size_t)o.H * 4);
+    case LEDE_T_QNET_W2: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qw2, (size_t)o.A * o.H * 4);
+    case LEDE_T_QNET_B2: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qb2, (size_t)o.A * 4);
+  }
+  return fail(c, LEDE_E_ARG, "unknown tensor kind %d", kind);
+}
+
+int lede_set_free_list(lede_ctx* c, const int32_t* order, int32_t n) {
+  if (!c || !order) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->table.empty()) return fail(c, LEDE_E_STATE, "pages are allocated");
+  if (n != c->lo.n_pages) return fail(c, LEDE_E_ARG, "order must list all %d pages", c->lo.n_pages);
+  std::vector<char> seen(n, 0);
+  for (int i = 0; i < n; ++i) {
+    if (order[i] < 0 || order[i] >= n || seen[order[i]]) return fail(c, LEDE_E_ARG, "order is not a permutation");
+    seen[order[i]] = 1;
+  }
+  c->free_list.assign(order, order + n);
+  return LEDE_OK;
+}
+
+int lede_set_options(lede_ctx* c, int32_t use_graphs, int32_t debug) {
+  if (!c) return LEDE_E_ARG;
+  c->use_graphs = use_graphs;
+  c->debug = debug;
+  return LEDE_OK;
+}
+
+int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token) {
+  if (!c || !tokens || n < 1) return fail(c, LEDE_E_ARG, "bad prefill arguments");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  for (int i = 0; i < n; ++i)
+    if (tokens[i] < 0 || tokens[i] >= c->lo.V) return fail(c, LEDE_E_ARG, "token %d out of range", tokens[i]);
+  hipStream_t s = S_(stream);
+  const int c0 = c->seq_len;
+  const size_t saved_table = c->table.size();
+  int rc = ensure_pages(c, c0 + n);
+  if (rc) return rc;
+  if ((rc = upload_table(c, s)) || (rc = upload_seq_len(c, c0, s))) { truncate_pages(c, c0); return rc; }
+  int32_t* pd = c->S<int32_t>(c->lo.prompt);
+  if (hipMemcpyAsync(pd, tokens, (size_t)n * 4, hipMemcpyHostToDevice, s) != hipSuccess) {
+    truncate_pages(c, c0);
+    return fail(c, LEDE_E_HIP, "prompt upload failed");
+  }
+  uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
+  int last_m = 0;
+  for (int off = 0; off < n; off += MROWS) {
+    const int M = std::min(MROWS, n - off);
+    TokenSrc tok{pd + off, nullptr};
+    rc = run_layers(c, M, false, tok, off, 0, c->lo.L, 0, vk, s);
+    if (!rc && off + M == n) rc = run_head(c, M, false, vk, verify_logits(c), s);
+    if (rc) { truncate_pages(c, c0); (void)saved_table; return rc; }
+    last_m = M;
+  }
+  c->last_rows = last_m;
+  HIP_CHECK(c, hipMemcpyAsync(c->keys_h, vk, MROWS * 8, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  const int next = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[last_m - 1] & 0xFFFFFFFFull));
+  HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, next, s));
+  rc = upload_seq_len(c, c0 + n, s);
+  if (rc) return rc;
+  c->seq_len = c0 + n;
+  c->pending = next;
+  if (next_token) *next_token = next;
+  return LEDE_OK;
+}
+
+int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
+  if (!c) return LEDE_E_ARG;
+  if (token < 0 || token >= c->lo.V) return fail(c, LEDE_E_ARG, "token out of range");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  hipStream_t s = S_(stream);
+  HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, token, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  c->pending = token;
+  return LEDE_OK;
+}
+
+int lede_truncate(lede_ctx* c, int32_t new_len, void* stream) {
+  if (!c) return LEDE_E_ARG;
+  if (new_len < 0 || new_len > c->seq_len) return fail(c, LEDE_E_ARG, "new_len %d not in [0, %d]", new_len, c->seq_len);
+  hipStream_t s = S_(stream);
+  truncate_pages(c, new_len);
+  c->drafted_k = -1;
+  int rc = upload_table(c, s);
+  if (rc) return rc;
+  rc = upload_seq_len(c, new_len, s);
+  if (rc) return rc;
+  c->seq_len = new_len;
+  return LEDE_OK;
+}
+
+static int draft_impl(lede_ctx* c, int l, int k, hipStream_t s) {
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is already outstanding");
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  if (l < 1 || l > c->lo.L) return fail(c, LEDE_E_ARG, "exit layer %d not in 1..%d", l, c->lo.L);
+  if (k < 1 || k > c->lo.k_max) return fail(c, LEDE_E_ARG, "draft length %d not in 1..%d", k, c->lo.k_max);
+  const size_t before = c->table.size();
+  int rc = ensure_pages(c, c->seq_len + k + 1);
+  if (rc) return rc;
+  if ((rc = upload_table(c, s))) { truncate_pages(c, c->seq_len); (void)before; return rc; }
+  rc = launch_drafts(c, l, 1, k, 0, 0, s);
+  if (rc) return rc;
+  c->drafted_k = k;
+  c->drafted_l = l;
+  return LEDE_OK;
+}
+
+int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts) {
+  if (!c) return LEDE_E_ARG;
+  hipStream_t s = S_(stream);
+  int rc = draft_impl(c, l, k, s);
+  if (rc) return rc;
+  if (drafts) {
+    HIP_CHECK(c, hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), 32 * 8, hipMemcpyDeviceToHost, s));
+    HIP_CHECK(c, hipStreamSynchronize(s));
+    for (int i = 0; i < k; ++i) drafts[i] = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[i + 1] & 0xFFFFFFFFull));
+  }
+  return LEDE_OK;
+}
+
+int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, int32_t* n_emitted, int32_t* verify) {
+  if (!c) return LEDE_E_ARG;
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  hipStream_t s = S_(stream);
+  const int k = c->drafted_k < 0 ? 0 : c->drafted_k;
+  if (c->drafted_k < 0) {
+    int rc = ensure_pages(c, c->seq_len + 1);
+    if (rc) return rc;
+    if ((rc = upload_table(c, s))) return rc;
+  }
+  int rc = launch_verify(c, k, s);
+  if (rc) return rc;
+  if (verify) HIP_CHECK(c, hipMemcpyAsync(c->keys_h + 16, c->S<uint64_t>(c->lo.vkeys), 16 * 8, hipMemcpyDeviceToHost, s));
+  rc = read_record(c, s);
+  if (rc) return rc;
+  commit_host(c);
+  const int a = c->record_h[0];
+  if (accepted) *accepted = a;
+  if (n_emitted) *n_emitted = a + 1;
+  if (tokens) for (int i = 0; i <= a; ++i) tokens[i] = c->record_h[4 + i];
+  if (verify) for (int i = 0; i <= k; ++i) verify[i] = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[16 + i] & 0xFFFFFFFFull));
+  return LEDE_OK;
+}
+
+int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, void* stream,
+              lede_step_record* rec) {
+  if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  const Layout& o = c->lo;
+  if (!forced && !o.H) return fail(c, LEDE_E_STATE, "no Q-network configured");
+  hipStream_t s = S_(stream);
+  memset(rec, 0, sizeof *rec);
+  rec->q_action = -1;
+  const int c0 = c->seq_len;
+  int l = forced ? forced->l : 0, k = forced ? forced->k : 0;
+  if (forced) {
+    if (l < 1 || l > o.L) return fail(c, LEDE_E_ARG, "exit layer %d not in 1..%d", l, o.L);
+    if (k < 0 || k > o.k_max) return fail(c, LEDE_E_ARG, "draft length %d not in 0..%d", k, o.k_max);
+  }
+  const int l_min = o.H ? c->cfg.exits[0] : 0;
+  const bool want_q = o.H && (!forced || log_qnet);
+  int k_eff = forced ? std::min(k, n_remaining - 1) : std::min(o.k_max, n_remaining - 1);
+  bool ran_q = false;
+  int rc;
+  if (k_eff > 0) {
+    if (!forced) {
+      // the agent decides at the first candidate layer of the first draft's
+      // forward pass; the step continues once its action is known
+      if ((rc = ensure_pages(c, c0 + 1)) || (rc = upload_table(c, s))) return rc;
+      uint64_t* dk = c->S<uint64_t>(o.dkeys);
+      rc = run_layers(c, 1, true, TokenSrc{nullptr, dk}, 0, 0, l_min, l_min, dk + 1, s);
+      if (rc) return rc;
+      HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
+      HIP_CHECK(c, hipStreamSynchronize(s));
+      const int a = c->record_h[48];
+      if (a < 0 || a >= o.A) return fail(c, LEDE_E_HIP, "Q-network action %d out of range", a);
+      l = c->cfg.exits[a / c->cfg.n_lengths];
+      k = c->cfg.lengths[a % c->cfg.n_lengths];
+      k_eff = std::min(std::min(k, o.k_max), n_remaining - 1);
+      ran_q = true;
+      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+      rc = launch_drafts(c, l, 1, k_eff, 0, l_min, s);
+      if (rc) return rc;
+    } else {
+      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+      const int qa = (want_q && l_min <= l) ? l_min : 0;
+      rc = launch_drafts(c, l, 1, k_eff, qa, 0, s);
+      if (rc) return rc;
+      ran_q = qa > 0;
+    }
+  } else {
+    k_eff = 0;
+    if ((rc = ensure_pages(c, c0 + 1)) || (rc = upload_table(c, s))) return rc;
+  }
+  rc = launch_verify(c, k_eff, s);
+  if (rc) return rc;
+  if (ran_q) HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
+  rc = read_record(c, s);
+  if (rc) return rc;
+  commit_host(c);
+  const int a = c->record_h[0];
+  rec->l = l;
+  rec->k_req = k;
+  rec->k_eff = k_eff;
+  rec->accepted = a;
+  rec->n_emitted = a + 1;
+  for (int i = 0; i <= a; ++i) rec->tokens[i] = c->record_h[4 + i];
+  for (int i = 0; i < k_eff; ++i) rec->drafts[i] = c->record_h[24 + i];
+  rec->seq_len = c->record_h[2];
+  rec->pending = c->record_h[3];
+  if (ran_q) {
+    rec->q_action = c->record_h[48];
+    int32_t bits = c->record_h[49];
+    memcpy(&rec->q_max, &bits, 4);
+  } else {
+    rec->q_max = NAN;
+  }
+  // Section 3.1.3 reward, summed over the drafts up to the first rejection
+  if (k_eff > 0) {
+    const double lam = (double)(o.L - l) / o.L;
+    rec->reward = (float)(a * (1.0 + lam) + (a < k_eff ? (-2.0 + lam) : 0.0));
+  }
+  return LEDE_OK;
+}
+
+int lede_get_kv_state(lede_ctx* c, int32_t* seq_len, int32_t* pending, int32_t* bt, int32_t cap, int32_t* n_table) {
+  if (!c) return LEDE_E_ARG;
+  if (seq_len) *seq_len = c->seq_len;
+  if (pending) *pending = c->pending;
+  if (n_table) *n_table = (int32_t)c->table.size();
+  if (bt) {
+    if (cap < (int)c->table.size()) return fail(c, LEDE_E_ARG, "block table capacity %d < %zu", cap, c->table.size());
+    for (size_t i = 0; i < c->table.size(); ++i) bt[i] = c->table[i];
+  }
+  return LEDE_OK;
+}
+
+int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t* rows, void* stream) {
+  if (!c || !host) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->debug) return fail(c, LEDE_E_STATE, "debug mode is off");
+  hipStream_t s = S_(stream);
+  const Layout& o = c->lo;
+  const float* src;
+  size_t n;
+  int r;
+  switch (which) {
+    case 0: r = c->last_rows; src = c->S<float>(o.logits); n = (size_t)r * o.V; break;
+    case 1: r = 1; src = c->S<float>(o.qv); n = (size_t)o.A; break;
+    case 2: r = 1; src = c->S<float>(o.qs); n = (size_t)o.d; break;
+    case 3: r = c->last_draft_rows; src = c->S<float>(o.logits) + (size_t)MROWS * o.V; n = (size_t)r * o.V; break;
+    default: return fail(c, LEDE_E_ARG, "unknown debug buffer %d", which);
+  }
+  if (cap < n) return fail(c, LEDE_E_ARG, "capacity %zu < %zu", cap, n);
+  HIP_CHECK(c, hipMemcpyAsync(host, src, n * 4, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  if (rows) *rows = r;
+  return LEDE_OK;
+}
+
+size_t lede_op_tiled_bytes(int32_t dtype, int32_t N, int32_t K) {
+  if ((dtype != 0 && dtype != 1) || N < 1 || K < 1) return 0;
+  return tiled_bytes(dtype, N, K);
+}
+
+int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* tiled, void* stream) {
+  if ((dtype != 0 && dtype != 1) || !src || !tiled || N < 1 || K < 1) return LEDE_E_ARG;
+  if (N % 16) return LEDE_E_UNSUPPORTED;
+  RepackArgs ra{};
+  ra.src = src; ra.N = N; ra.K = K; ra.dst = tiled; ra.KT = k_tiles(dtype, K);
+  ra.group0 = 0; ra.n_groups = N / 16; ra.order = ROWS_PLAIN; ra.hd = 0;
+  return launch_repack(dtype, ra, S_(stream)) == hipSuccess ? LEDE_OK : LEDE_E_HIP;
+}
+
+int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M, float* y,
+                   int32_t use_mfma, void* stream) {
+  if ((dtype != 0 && dtype != 1) || !tiled || !x || !y || N < 1 || K < 1) return LEDE_E_ARG;
+  if (N % 16 || K % tile_k(dtype)) return LEDE_E_UNSUPPORTED;
+  if (M < 1 || M > 16 || (!use_mfma && M != 1)) return LEDE_E_ARG;
+  LinearArgs a{};
+  a.w = (const uint8_t*)tiled;
+  a.n_groups = N / 16; a.KT = k_tiles(dtype, K); a.K = K; a.M = M;
+  a.x_mode = X_PLAIN; a.x = x; a.ldx = K;
+  a.epi = EPI_STORE; a.out = y; a.ldo = N;
+  return launch_linear(dtype, use_mfma != 0, a, std::min(a.n_groups, 4096), S_(stream)) == hipSuccess ? LEDE_OK
+                                                                                                  : LEDE_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,297 @@
+"""Thin ctypes binding of liblede (include/lede.h).
+
+Argument marshalling only: every step of decoding runs in the library's HIP
+kernels.  PyTorch provides device memory (the weight arena, KV pool,
+workspace and weight staging buffers) and the stream handle.  There is no
+fallback: if liblede.so is missing or no GPU is present, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblede.so")
+
+LEDE_OK, LEDE_E_ARG, LEDE_E_STATE, LEDE_E_KV_FULL, LEDE_E_CTX_OVERFLOW, LEDE_E_HIP, LEDE_E_UNSUPPORTED = \
+    0, -1, -2, -3, -4, -5, -6
+STATUS = {0: "OK", -1: "E_ARG", -2: "E_STATE", -3: "E_KV_FULL", -4: "E_CTX_OVERFLOW", -5: "E_HIP",
+          -6: "E_UNSUPPORTED"}
+
+T_EMBED, T_FINAL_NORM, T_HEAD, T_ATTN_NORM, T_WQ, T_WK, T_WV, T_WO, T_FFN_NORM, T_WG, T_WU, T_WD, \
+    T_QNET_W1, T_QNET_B1, T_QNET_W2, T_QNET_B2 = range(16)
+LAYER_KINDS = {"attn_norm": T_ATTN_NORM, "wq": T_WQ, "wk": T_WK, "wv": T_WV, "wo": T_WO,
+               "ffn_norm": T_FFN_NORM, "wg": T_WG, "wu": T_WU, "wd": T_WD}
+
+
+class LedeConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_float),
+                ("dtype", ctypes.c_int32), ("max_ctx", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("n_pages", ctypes.c_int32), ("qnet_hidden", ctypes.c_int32), ("n_exits", ctypes.c_int32),
+                ("n_lengths", ctypes.c_int32), ("exits", ctypes.c_int32 * 64), ("lengths", ctypes.c_int32 * 16),
+                ("k_max", ctypes.c_int32)]
+
+
+class LedeAction(ctypes.Structure):
+    _fields_ = [("l", ctypes.c_int32), ("k", ctypes.c_int32)]
+
+
+class LedeStepRecord(ctypes.Structure):
+    _fields_ = [("l", ctypes.c_int32), ("k_req", ctypes.c_int32), ("k_eff", ctypes.c_int32),
+                ("accepted", ctypes.c_int32), ("n_emitted", ctypes.c_int32), ("tokens", ctypes.c_int32 * 17),
+                ("drafts", ctypes.c_int32 * 16), ("q_action", ctypes.c_int32), ("q_max", ctypes.c_float),
+                ("reward", ctypes.c_float), ("seq_len", ctypes.c_int32), ("pending", ctypes.c_int32)]
+
+
+EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error", "lede_load_tensor",
+            "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
+            "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
+            "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear"]
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load liblede.so and declare its signatures.  Raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("liblede.so not built (run __graft_entry__.build()): %s" % path)
+    L = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    P = ctypes.POINTER
+    L.lede_region_bytes.argtypes = [P(LedeConfig), P(sz), P(sz), P(sz)]
+    L.lede_create.argtypes = [P(LedeConfig), vp, sz, vp, sz, vp, sz, P(vp)]
+    L.lede_destroy.argtypes = [vp]
+    L.lede_destroy.restype = None
+    L.lede_last_error.argtypes = [vp]
+    L.lede_last_error.restype = ctypes.c_char_p
+    L.lede_load_tensor.argtypes = [vp, i32, i32, vp, vp]
+    L.lede_set_free_list.argtypes = [vp, P(i32), i32]
+    L.lede_set_options.argtypes = [vp, i32, i32]
+    L.lede_prefill.argtypes = [vp, P(i32), i32, vp, P(i32)]
+    L.lede_set_pending.argtypes = [vp, i32, vp]
+    L.lede_truncate.argtypes = [vp, i32, vp]
+    L.lede_draft.argtypes = [vp, i32, i32, vp, P(i32)]
+    L.lede_verify.argtypes = [vp, vp, P(i32), P(i32), P(i32), P(i32)]
+    L.lede_step.argtypes = [vp, P(LedeAction), i32, i32, vp, P(LedeStepRecord)]
+    L.lede_get_kv_state.argtypes = [vp, P(i32), P(i32), P(i32), i32, P(i32)]
+    L.lede_debug_read.argtypes = [vp, i32, P(ctypes.c_float), sz, P(i32), vp]
+    L.lede_op_tiled_bytes.argtypes = [i32, i32, i32]
+    L.lede_op_tiled_bytes.restype = sz
+    L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
+    L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, vp, i32, vp]
+    for name in EXPORTED:
+        if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes"):
+            getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+class LedeError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__("%s (%d): %s" % (STATUS.get(code, "?"), code, msg))
+        self.code = code
+
+
+def make_config(model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15) -> LedeConfig:
+    """lede_config from a model shape (any object with the ModelConfig fields)."""
+    c = LedeConfig()
+    c.n_layers, c.d_model, c.n_heads = model.n_layers, model.d_model, model.n_heads
+    c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab = model.n_kv_heads, model.head_dim, model.ffn_dim, model.vocab
+    c.rms_eps, c.rope_base = model.rms_eps, model.rope_base
+    c.dtype = 1 if model.dtype == "bf16" else 0
+    c.max_ctx, c.page_size = max_ctx, 64
+    c.n_pages = n_pages if n_pages is not None else -(-max_ctx // 64)
+    c.qnet_hidden = model.qnet_hidden
+    c.n_exits, c.n_lengths = len(model.exits), len(model.lengths)
+    for i, e in enumerate(model.exits):
+        c.exits[i] = e
+    for i, k in enumerate(model.lengths):
+        c.lengths[i] = k
+    c.k_max = k_max
+    return c
+
+
+def _i32p(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+@dataclass
+class StepRecord:
+    l: int
+    k_req: int
+    k_eff: int
+    accepted: int
+    emitted: List[int]
+    drafts: List[int]
+    q_action: int
+    q_max: float
+    reward: float
+    seq_len: int
+    pending: int
+
+
+class Engine:
+    """A liblede context over torch-allocated device regions."""
+
+    def __init__(self, model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15, device: int = 0):
+        import torch
+        self.torch = torch
+        self.L = load()
+        self.model = model
+        self.cfg = make_config(model, max_ctx, n_pages, k_max)
+        wb, kvb, wsb = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+        self._check(self.L.lede_region_bytes(ctypes.byref(self.cfg), ctypes.byref(wb), ctypes.byref(kvb),
+                                             ctypes.byref(wsb)), None)
+        self.region_bytes = (wb.value, kvb.value, wsb.value)
+        dev = torch.device("cuda", device)
+        self.device = dev
+        self.weights = torch.empty(wb.value, dtype=torch.uint8, device=dev)
+        self.kv = torch.empty(kvb.value, dtype=torch.uint8, device=dev)
+        self.ws = torch.empty(wsb.value, dtype=torch.uint8, device=dev)
+        h = ctypes.c_void_p()
+        self._check(self.L.lede_create(ctypes.byref(self.cfg), self.weights.data_ptr(), wb.value,
+                                       self.kv.data_ptr(), kvb.value, self.ws.data_ptr(), wsb.value,
+                                       ctypes.byref(h)), None)
+        self.ctx = h
+
+    # -- plumbing ----------------------------------------------------------
+    @property
+    def stream(self):
+        return ctypes.c_void_p(self.torch.cuda.current_stream(self.device).cuda_stream)
+
+    def _check(self, rc: int, ctx):
+        if rc != LEDE_OK:
+            msg = self.L.lede_last_error(ctx).decode() if ctx is not None else ""
+            raise LedeError(rc, msg)
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            self.L.lede_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- weights -------------------------------------------------------------
+    def load_tensor(self, kind: int, layer: int, host: np.ndarray):
+        t = self.torch
+        a = np.ascontiguousarray(host)
+        if a.dtype == np.uint16:
+            a = a.view(np.int16)
+        dev = t.from_numpy(a).to(self.device)
+        self._check(self.L.lede_load_tensor(self.ctx, kind, layer, dev.data_ptr(), self.stream), self.ctx)
+        t.cuda.current_stream(self.device).synchronize()
+
+    def load_weights(self, weights: dict, qnet: Optional[dict] = None):
+        """weights: lede_inputs.weights() layout; qnet: lede_inputs.qnet_weights()."""
+        self.load_tensor(T_EMBED, 0, weights["embed"])
+        self.load_tensor(T_FINAL_NORM, 0, weights["final_norm"])
+        self.load_tensor(T_HEAD, 0, weights["head"])
+        for j, lw in enumerate(weights["layers"]):
+            for name, kind in LAYER_KINDS.items():
+                self.load_tensor(kind, j, lw[name])
+        if qnet is not None:
+            for name, kind in (("w1", T_QNET_W1), ("b1", T_QNET_B1), ("w2", T_QNET_W2), ("b2", T_QNET_B2)):
+                self.load_tensor(kind, 0, qnet[name])
+
+    # -- C-ABI calls (same names) --------------------------------------------------
+    def lede_set_options(self, use_graphs: int = 0, debug: int = 0):
+        self._check(self.L.lede_set_options(self.ctx, use_graphs, debug), self.ctx)
+
+    def lede_set_free_list(self, order: Sequence[int]):
+        a = np.ascontiguousarray(order, dtype=np.int32)
+        self._check(self.L.lede_set_free_list(self.ctx, _i32p(a), len(a)), self.ctx)
+
+    def lede_prefill(self, tokens: Sequence[int]) -> int:
+        a = np.ascontiguousarray(tokens, dtype=np.int32)
+        nxt = ctypes.c_int32()
+        self._check(self.L.lede_prefill(self.ctx, _i32p(a), len(a), self.stream, ctypes.byref(nxt)), self.ctx)
+        return nxt.value
+
+    def lede_set_pending(self, token: int):
+        self._check(self.L.lede_set_pending(self.ctx, token, self.stream), self.ctx)
+
+    def lede_truncate(self, new_len: int):
+        self._check(self.L.lede_truncate(self.ctx, new_len, self.stream), self.ctx)
+
+    def lede_draft(self, l: int, k: int, read: bool = True) -> Optional[List[int]]:
+        out = np.zeros(max(k, 1), dtype=np.int32)
+        self._check(self.L.lede_draft(self.ctx, l, k, self.stream, _i32p(out) if read else None), self.ctx)
+        return [int(x) for x in out[:k]] if read else None
+
+    def lede_verify(self):
+        """Returns (accepted, emitted tokens, verify argmax of every row)."""
+        acc, ne = ctypes.c_int32(), ctypes.c_int32()
+        toks = np.zeros(17, dtype=np.int32)
+        ver = np.zeros(17, dtype=np.int32)
+        self._check(self.L.lede_verify(self.ctx, self.stream, ctypes.byref(acc), _i32p(toks), ctypes.byref(ne),
+                                       _i32p(ver)), self.ctx)
+        return acc.value, [int(x) for x in toks[:ne.value]], ver
+
+    def lede_step(self, action=None, n_remaining: int = 1 << 30, log_qnet: bool = True) -> StepRecord:
+        rec = LedeStepRecord()
+        act = LedeAction(int(action[0]), int(action[1])) if action is not None else None
+        self._check(self.L.lede_step(self.ctx, ctypes.byref(act) if act is not None else None, int(log_qnet),
+                                     int(n_remaining), self.stream, ctypes.byref(rec)), self.ctx)
+        return StepRecord(l=rec.l, k_req=rec.k_req, k_eff=rec.k_eff, accepted=rec.accepted,
+                          emitted=[rec.tokens[i] for i in range(rec.n_emitted)],
+                          drafts=[rec.drafts[i] for i in range(rec.k_eff)], q_action=rec.q_action,
+                          q_max=rec.q_max, reward=rec.reward, seq_len=rec.seq_len, pending=rec.pending)
+
+    def lede_get_kv_state(self):
+        """(seq_len, pending, block table)."""
+        sl, pend, n = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        cap = self.cfg.max_ctx // 64 + 2
+        bt = np.zeros(cap, dtype=np.int32)
+        self._check(self.L.lede_get_kv_state(self.ctx, ctypes.byref(sl), ctypes.byref(pend), _i32p(bt), cap,
+                                             ctypes.byref(n)), self.ctx)
+        return sl.value, pend.value, [int(x) for x in bt[:n.value]]
+
+    def lede_debug_read(self, which: int, n_floats: int) -> np.ndarray:
+        out = np.zeros(n_floats, dtype=np.float32)
+        rows = ctypes.c_int32()
+        self._check(self.L.lede_debug_read(self.ctx, which, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                           n_floats, ctypes.byref(rows), self.stream), self.ctx)
+        return out, rows.value
+
+    def logits(self, which: int = 0) -> np.ndarray:
+        """Debug logits of the last verify/prefill head (which=0) or of the
+        last draft passes (which=3), shape [rows][vocab]."""
+        V = self.model.vocab
+        out, rows = self.lede_debug_read(which, 16 * V)
+        return out[:rows * V].reshape(rows, V)
+
+
+# ---- single-op helpers (kernel-level tests) ----------------------------------------
+
+def op_linear(W, x, use_mfma: bool):
+    """y = x W^T through the library's tiled linear kernels.  W [N][K] and x
+    [M][K] are torch tensors on the GPU (float32 or bfloat16)."""
+    import torch
+    L = load()
+    dtype = 1 if W.dtype == torch.bfloat16 else 0
+    N, K = W.shape
+    M = x.shape[0]
+    tiled = torch.empty(L.lede_op_tiled_bytes(dtype, N, K), dtype=torch.uint8, device=W.device)
+    y = torch.empty(M, N, dtype=torch.float32, device=W.device)
+    s = ctypes.c_void_p(torch.cuda.current_stream(W.device).cuda_stream)
+    rc = L.lede_op_repack(dtype, W.data_ptr(), N, K, tiled.data_ptr(), s)
+    if rc:
+        raise LedeError(rc, "op_repack")
+    rc = L.lede_op_linear(dtype, tiled.data_ptr(), N, K, x.contiguous().data_ptr(), M, y.data_ptr(),
+                          int(use_mfma), s)
+    if rc:
+        raise LedeError(rc, "op_linear")
+    return y

@@ -1,0 +1,80 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point include/lede.h declares, and validates configurations."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import lede_inputs as li
+from lede_inputs.configs import WORKLOADS, TINY, shrink
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2606_03113_amd import lede
+    if not os.path.exists(lede.LIB_PATH):
+        from paper_2606_03113_amd import build
+        build.build()
+    return lede.load()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "lede.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lede_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 18
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_binding_names_match_header():
+    from paper_2606_03113_amd import lede
+    assert sorted(lede.EXPORTED) == declared_functions()
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_region_bytes_for_every_workload(lib, name):
+    from paper_2606_03113_amd import lede
+    w = WORKLOADS[name]
+    m = w.model
+    cfg = lede.make_config(m, w.max_ctx)
+    wb, kvb, wsb = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.lede_region_bytes(ctypes.byref(cfg), ctypes.byref(wb), ctypes.byref(kvb), ctypes.byref(wsb)) == 0
+    model_bytes = m.n_layers * m.layer_weight_bytes() + m.head_weight_bytes() + m.vocab * m.d_model * m.wbytes
+    assert model_bytes <= wb.value <= model_bytes * 1.02 + (1 << 20) + m.qnet_bytes() * 2
+    pages = -(-w.max_ctx // 64)
+    assert kvb.value >= 2 * m.n_layers * pages * 64 * m.kv_dim * m.wbytes
+
+
+@pytest.mark.parametrize("bad", [dict(head_dim=96, d_model=384), dict(ffn_dim=690), dict(vocab=1000),
+                                 dict(n_kv_heads=3)])
+def test_unsupported_shapes_are_rejected(lib, bad):
+    from paper_2606_03113_amd import lede
+    m = shrink(TINY, **bad)
+    cfg = lede.make_config(m, 128)
+    wb = ctypes.c_size_t()
+    assert lib.lede_region_bytes(ctypes.byref(cfg), ctypes.byref(wb), None, None) == lede.LEDE_E_UNSUPPORTED
+
+
+def test_bad_page_size_and_kmax_rejected(lib):
+    from paper_2606_03113_amd import lede
+    cfg = lede.make_config(TINY, 128)
+    cfg.page_size = 32
+    assert lib.lede_region_bytes(ctypes.byref(cfg), None, None, None) == lede.LEDE_E_UNSUPPORTED
+    cfg = lede.make_config(TINY, 128, k_max=16)
+    assert lib.lede_region_bytes(ctypes.byref(cfg), None, None, None) == lede.LEDE_E_UNSUPPORTED
+
+
+def test_null_arguments(lib):
+    from paper_2606_03113_amd import lede
+    assert lib.lede_region_bytes(None, None, None, None) == lede.LEDE_E_ARG
+    out = ctypes.c_void_p()
+    assert lib.lede_create(None, None, 0, None, 0, None, 0, ctypes.byref(out)) == lede.LEDE_E_ARG
+    assert lib.lede_last_error(None) == b"null context"

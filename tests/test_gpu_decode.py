@@ -1,0 +1,191 @@
+"""End-to-end parity of the GPU decode path (prefill, draft, verify, accept,
+KV truncation, Q-network) against the CPU oracle on small Llama-style models
+that still span several tiles, two KV pages and ragged tails.  Run through
+the C ABI (ctypes binding)."""
+import numpy as np
+import pytest
+
+import lede_inputs as li
+from lede_inputs.configs import TINY, WORKLOADS, shrink
+from oracle.model import SSDState, greedy_ar
+from tests.parity import Report, check_ar, check_ssd, make_decoder, say
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+TINY_BF16 = shrink(TINY, name="tiny-bf16", dtype="bf16")
+SMALL_128 = shrink(TINY, name="small-hd128-bf16", n_layers=3, d_model=512, n_heads=4, n_kv_heads=4,
+                   head_dim=128, ffn_dim=1376, vocab=4096, dtype="bf16", qnet_hidden=64,
+                   exits=(1, 2, 3), lengths=tuple(range(1, 9)))
+SMALL_GQA = shrink(TINY, name="small-gqa-bf16", n_layers=3, d_model=512, n_heads=8, n_kv_heads=2,
+                   head_dim=64, ffn_dim=1408, vocab=2048, dtype="bf16", rope_base=500000.0,
+                   qnet_hidden=32, exits=(1, 2, 3), lengths=(1, 2, 4, 8))
+GQA_128 = shrink(TINY, name="gqa-hd128-f32", n_layers=2, d_model=512, n_heads=8, n_kv_heads=2,
+                 head_dim=128, ffn_dim=704, vocab=1024, dtype="f32", qnet_hidden=32,
+                 exits=(1, 2), lengths=(1, 3, 5))
+MODELS = [TINY, TINY_BF16, SMALL_128, SMALL_GQA, GQA_128]
+
+PROMPT = 70      # crosses the first 64-token page
+N_GEN = 40
+
+
+def _engine(model, max_ctx=160, n_pages=None, order=None):
+    from paper_2606_03113_amd import Engine
+    eng = Engine(model, max_ctx=max_ctx, n_pages=n_pages, k_max=8)
+    w = li.weights(model)
+    q = li.qnet_weights(model)
+    eng.load_weights(w, q)
+    eng.lede_set_options(0, 1)
+    if order is not None:
+        eng.lede_set_free_list(order)
+    return eng, w, q
+
+
+def _prompt(model, n=PROMPT):
+    return li.uniform_int(1, 20, n, 0, model.vocab - 1)
+
+
+@pytest.mark.parametrize("model", MODELS, ids=lambda m: m.name)
+def test_prefill_and_ar_decode(model):
+    say("ar parity", model.name)
+    eng, w, q = _engine(model)
+    dec = make_decoder(model, w, q, 160)
+    rep = Report()
+    check_ar(eng, dec, model, _prompt(model), 24, rep)
+    say("  rows=%d max_err/tol=%.3g abs=%.3g subs=%d" % (rep.rows, rep.max_err_rel, rep.max_err_abs,
+                                                         rep.substitutions))
+
+
+@pytest.mark.parametrize("model", MODELS, ids=lambda m: m.name)
+def test_ssd_fixed_and_schedule(model):
+    say("ssd parity", model.name)
+    n_pages = 6
+    order = list(np.random.default_rng(5).permutation(n_pages))
+    eng, w, q = _engine(model, n_pages=n_pages, order=order)
+    dec = make_decoder(model, w, q, 160)
+    st = SSDState(dec, n_pages, 64, order)
+    prompt = _prompt(model)
+    g = eng.lede_prefill(prompt)
+    st.prefill(prompt)
+    rep = Report()
+    if g != st.pending:
+        rep.token(model.dtype, g, dec.head(dec.forward(prompt, 0, model.n_layers)[-1:])[0])
+        eng.lede_set_pending(st.pending)
+    L = model.n_layers
+    acts = [(1, 3), (L, 4), (2 if L > 2 else 1, 8), (1, 1), (L, 8)]
+    sched = np.stack([li.uniform_int(2, 30, 64, 1, L), li.uniform_int(2, 31, 64, 1, 8)], 1)
+    check_ssd(eng, st, model, 1 + 14, acts, rep, qnet_log=True)
+    check_ssd(eng, st, model, 1 + 14 + 20, sched, rep, qnet_log=False)
+    say("  steps=%d rows=%d max_err/tol=%.3g subs=%d" % (rep.steps, rep.rows, rep.max_err_rel, rep.substitutions))
+
+
+@pytest.mark.parametrize("model", [TINY, SMALL_128, SMALL_GQA], ids=lambda m: m.name)
+def test_qnet_policy(model):
+    say("qnet policy", model.name)
+    eng, w, q = _engine(model)
+    dec = make_decoder(model, w, q, 160)
+    st = SSDState(dec, 3, 64)
+    prompt = _prompt(model)
+    g = eng.lede_prefill(prompt)
+    st.prefill(prompt)
+    rep = Report()
+    if g != st.pending:
+        rep.token(model.dtype, g, dec.head(dec.forward(prompt, 0, model.n_layers)[-1:])[0])
+        eng.lede_set_pending(st.pending)
+    check_ssd(eng, st, model, 30, [(1, 1)], rep, qnet_policy=True)
+    say("  steps=%d subs=%d" % (rep.steps, rep.substitutions))
+
+
+@pytest.mark.parametrize("model", [TINY_BF16, SMALL_128, SMALL_GQA], ids=lambda m: m.name)
+def test_gpu_ssd_equals_gpu_ar_bitwise(model):
+    """Greedy self-speculative output equals greedy autoregressive output on
+    the GPU itself, bit for bit (the verify path is row-independent)."""
+    say("ssd == ar on gpu", model.name)
+    prompt = _prompt(model)
+    eng, w, q = _engine(model)
+    eng.lede_set_options(0, 0)
+    ar = [eng.lede_prefill(prompt)]
+    while len(ar) < N_GEN:
+        a, em, _ = eng.lede_verify()
+        ar += em
+    for act in [(1, 4), (model.n_layers, 6), (2, 8)]:
+        eng2, _, _ = _engine(model)
+        eng2.lede_set_options(0, 0)
+        out = [eng2.lede_prefill(prompt)]
+        while len(out) < N_GEN:
+            rec = eng2.lede_step(act, n_remaining=N_GEN - len(out))
+            out += rec.emitted
+        assert out == ar, act
+        if act[0] == model.n_layers:
+            pass  # drafts at l = L use the vector kernels; acceptance may still differ by rounding
+
+
+def test_zeroed_upper_layers_accept_all_on_gpu():
+    model = TINY_BF16
+    from paper_2606_03113_amd import Engine
+    eng = Engine(model, max_ctx=160, k_max=8)
+    w = li.weights(model)
+    for j in range(2, model.n_layers):
+        w["layers"][j]["wo"] = np.zeros_like(w["layers"][j]["wo"])
+        w["layers"][j]["wd"] = np.zeros_like(w["layers"][j]["wd"])
+    eng.load_weights(w, li.qnet_weights(model))
+    say("zeroed upper layers", model.name)
+    eng.lede_prefill(_prompt(model))
+    acc = drafted = 0
+    for _ in range(8):
+        rec = eng.lede_step((2, 6), n_remaining=100)
+        acc += rec.accepted
+        drafted += rec.k_eff
+    # drafts at layer 2 see the same hidden state as the full model; the
+    # vector and matrix kernels round differently, so allow rare near-ties
+    assert acc >= drafted - 2, (acc, drafted)
+
+
+def test_error_paths_leave_state_unchanged():
+    from paper_2606_03113_amd.lede import LedeError, LEDE_E_ARG, LEDE_E_STATE, LEDE_E_CTX_OVERFLOW, \
+        LEDE_E_KV_FULL
+    model = TINY
+    say("error paths", model.name)
+    eng, w, q = _engine(model, max_ctx=100, n_pages=2)
+    with pytest.raises(LedeError) as e:
+        eng.lede_verify()
+    assert e.value.code == LEDE_E_STATE
+    eng.lede_prefill(_prompt(model, 60))
+    before = eng.lede_get_kv_state()
+    for bad in [(0, 2), (model.n_layers + 1, 2), (2, 9), (2, -1)]:
+        with pytest.raises(LedeError) as e:
+            eng.lede_step(bad, n_remaining=50)
+        assert e.value.code == LEDE_E_ARG
+        assert eng.lede_get_kv_state() == before
+    with pytest.raises(LedeError) as e:
+        eng.lede_draft(2, 0)
+    assert e.value.code == LEDE_E_ARG
+    eng.lede_draft(2, 3)
+    with pytest.raises(LedeError) as e:
+        eng.lede_draft(2, 3)
+    assert e.value.code == LEDE_E_STATE
+    with pytest.raises(LedeError) as e:
+        eng.lede_step((2, 3), n_remaining=50)
+    assert e.value.code == LEDE_E_STATE
+    a, em, _ = eng.lede_verify()
+    assert eng.lede_get_kv_state()[0] == 60 + a + 1
+    with pytest.raises(LedeError) as e:
+        eng.lede_truncate(1000)
+    assert e.value.code == LEDE_E_ARG
+    # context overflow: 100 positions at most
+    sl = eng.lede_get_kv_state()[0]
+    with pytest.raises(LedeError) as e:
+        eng.lede_prefill([1] * (100 - sl + 1))
+    assert e.value.code == LEDE_E_CTX_OVERFLOW
+    assert eng.lede_get_kv_state()[0] == sl
+    # KV pool of 2 pages: a third page is refused
+    eng3, _, _ = _engine(model, max_ctx=256, n_pages=2)
+    eng3.lede_prefill(_prompt(model, 120))
+    st = eng3.lede_get_kv_state()
+    with pytest.raises(LedeError) as e:
+        eng3.lede_prefill([1] * 10)
+    assert e.value.code == LEDE_E_KV_FULL
+    assert eng3.lede_get_kv_state() == st
+    with pytest.raises(LedeError) as e:
+        eng3.lede_set_pending(model.vocab)
+    assert e.value.code == LEDE_E_ARG
