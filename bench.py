@@ -1,0 +1,238 @@
+"""Decode throughput of batch-1 self-speculative decoding on one MI355X.
+
+Workload (default): the Llama-2-7B-shaped random-init bf16 decoder, a
+512-token uniform-random prompt, 256 generated tokens, static exit layer
+l = 8 and draft length k = 4 (the Q-network is evaluated and logged every
+step).  A step is one pass of the whole hot path: Q-network, k draft passes
+through layers 1..l with the shared final norm + LM head + argmax, one
+(k+1)-row verify pass through all L layers, greedy acceptance, KV
+truncation.  Inputs are synthetic and already resident in HBM when timing
+starts.
+
+Prints one JSON line: tokens/s over the timed steps, the HBM roofline of the
+dominant kernel (algorithmic bytes / HIP-event duration, from a second,
+instrumented replay of the same steps) and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pass_bytes(m, l, c):
+    """Algorithmic bytes of one draft pass through l layers at KV length c."""
+    kv = m.kv_bytes_per_token_layer()
+    return l * m.layer_weight_bytes() + m.head_weight_bytes() + l * (c + 1) * kv
+
+
+def verify_bytes(m, k, c):
+    kv = m.kv_bytes_per_token_layer()
+    return m.n_layers * m.layer_weight_bytes() + m.head_weight_bytes() + m.n_layers * (c + k + 1) * kv
+
+
+def kernel_source_sha():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        h.update(open(os.path.join(ROOT, "paper_2606_03113_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel_name, workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel_name, workload))
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    if d.get("kernel_src_sha") != kernel_source_sha():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
+    """The CPU oracle on a bounded sample: SSD steps at the workload's action
+    from KV length = prompt length, with the prompt's KV cache filled with
+    synthetic bf16 values instead of an oracle prefill."""
+    from oracle.model import OracleDecoder, SSDState
+    m = wl.model
+    P = wl.prompt_len
+    max_ctx = P + 64
+    dec = OracleDecoder(m, weights, max_ctx, qnet)
+    rng = np.random.default_rng(0)
+    for cache in (dec.kcache, dec.vcache):
+        vals = rng.standard_normal((m.n_layers, P, m.kv_dim)).astype(np.float32)
+        cache[:, :P, :] = (vals.view(np.uint32) & 0xFFFF0000).view(np.float32)
+    st = SSDState(dec, -(-max_ctx // 64), 64)
+    st.pager.ensure(P)
+    st.c, st.pending, st.out = P, prompt_next, [prompt_next]
+    l, k = wl.fixed
+    t0 = time.time()
+    toks = steps = 0
+    while steps < max_steps and (steps < 2 or time.time() - t0 < budget_s):
+        rec = st.step(l, k, wl.n_gen, qnet=m.qnet_hidden > 0)
+        toks += len(rec.emitted)
+        steps += 1
+    el = time.time() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": toks / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "%d SSD steps (l=%d, k=%d) of %s from KV length %d (prompt KV filled with synthetic "
+                      "bf16 values, no oracle prefill); %.1f s" % (steps, l, k, wl.name, P, el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama2-7b")
+    ap.add_argument("--l", type=int, default=None)
+    ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--prof-steps", type=int, default=30)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graphs", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (see the sharding "
+              "design notes); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import lede_inputs as li
+    from lede_inputs.configs import WORKLOADS
+    from paper_2606_03113_amd import Engine
+
+    wl = WORKLOADS[args.workload]
+    m = wl.model
+    l, k = wl.fixed
+    if args.l is not None or args.k is not None:
+        from dataclasses import replace
+        l = args.l if args.l is not None else l
+        k = args.k if args.k is not None else k
+        wl = replace(wl, fixed=(l, k))
+    t0 = time.time()
+    log("generating %s weights ..." % m.name)
+    weights = li.weights(m)
+    qnet = li.qnet_weights(m) if m.qnet_hidden else None
+    prompt = li.prompt(wl)
+    log("  %.1f s" % (time.time() - t0))
+    eng = Engine(m, max_ctx=wl.max_ctx, k_max=max(8, k))
+    eng.load_weights(weights, qnet)
+    eng.lede_set_options(args.graphs, 0)
+    log("weights resident (%.1f GB arena)  %.1f s" % (eng.region_bytes[0] / 1e9, time.time() - t0))
+    first = eng.lede_prefill(prompt)
+    log("prefill %d tokens done  %.1f s" % (wl.prompt_len, time.time() - t0))
+
+    produced = [first]
+    log_q = m.qnet_hidden > 0
+
+    def step():
+        rec = eng.lede_step((l, k), n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
+        produced.extend(rec.emitted)
+        return rec
+
+    if args.warmup + args.steps >= wl.n_gen - 1:
+        sys.exit("warmup + steps must stay below the %d generated tokens" % wl.n_gen)
+    for _ in range(args.warmup):
+        step()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    n0 = len(produced)
+    recs = []
+    w0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        recs.append(step())
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1)
+    toks = len(produced) - n0
+    log("timed %d steps: %.3f ms/step (wall %.3f ms/step), %d tokens" % (args.steps, ms / args.steps,
+                                                                        1e3 * wall / args.steps, toks))
+
+    # instrumented replay of the same steps from the prompt state
+    eng.lede_truncate(wl.prompt_len)
+    eng.lede_set_pending(first)
+    del produced[1:]
+    for _ in range(min(args.warmup, 3)):
+        step()
+    eng.lede_prof_enable(True)
+    eng.lede_prof_read(reset=True)
+    prof_recs = [step() for _ in range(args.prof_steps)]
+    prof = eng.lede_prof_read(reset=True)
+    eng.lede_prof_enable(False)
+    lin = {n: prof[n] for n in ("linear_vec", "linear_mfma")}
+    dom = max(lin, key=lambda n: lin[n]["ms"])
+    d = lin[dom]
+    achieved = d["bytes"] / (d["ms"] * 1e6)  # GB/s
+    kname = {"linear_vec": "k_linear_bf16_vec", "linear_mfma": "k_linear_bf16_mfma"}[dom]
+    traffic = traffic_from_profile(kname, wl.name)
+    dp, vp = prof["draft_phase"], prof["verify_phase"]
+    # algorithmic bytes of the instrumented steps' passes
+    db = vb = 0.0
+    for r in prof_recs:
+        c = r.seq_len - r.accepted - 1  # KV length when the step started
+        db += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff)) + (m.qnet_bytes() if log_q else 0)
+        vb += verify_bytes(m, r.k_eff, c)
+    acc_tokens = sum(len(r.emitted) for r in recs)
+    accepted = sum(r.accepted for r in recs)
+    drafted = sum(r.k_eff for r in recs)
+    out = {
+        "metric": "decode tokens/s (batch 1, SSD) + % of HBM peak, Llama-2-7B-shaped bf16"
+        if wl.name == "llama2-7b" else "decode tokens/s (batch 1, SSD), %s" % wl.name,
+        "value": round(acc_tokens / (ms / 1e3), 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": m.dtype,
+        "data": "synthetic (random-init N(0,0.02) weights, uniform-random prompt)",
+        "config": {"workload": "%s: L=%d d=%d heads=%d/%d ffn=%d vocab=%d, prompt %d, generate %d, "
+                               "static exit l=%d, draft k=%d, Q-network logged" %
+                               (m.name, m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.ffn_dim, m.vocab,
+                                wl.prompt_len, wl.n_gen, l, k),
+                   "batch": 1, "prompt_len": wl.prompt_len, "exit_layer": l, "draft_len": k,
+                   "graphs": bool(args.graphs)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": kname,
+                     "avg_launch_us": round(1e3 * d["ms"] / max(d["launches"], 1), 3),
+                     "launches": d["launches"]},
+        "passes": {
+            "draft_GBps": round(db / (dp["ms"] * 1e6), 1) if dp["ms"] else None,
+            "verify_GBps": round(vb / (vp["ms"] * 1e6), 1) if vp["ms"] else None,
+            "draft_frac": round(db / (dp["ms"] * 1e6) / HBM_PEAK_GBPS, 4) if dp["ms"] else None,
+            "verify_frac": round(vb / (vp["ms"] * 1e6) / HBM_PEAK_GBPS, 4) if vp["ms"] else None,
+            "kernel_ms": {n: round(v["ms"] / args.prof_steps, 4) for n, v in prof.items()},
+        },
+        "acceptance": {"accepted": accepted, "drafted": drafted,
+                       "acc_rate": round(accepted / drafted, 4) if drafted else None},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(wl, weights, qnet, first)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

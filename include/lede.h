@@ -193,6 +193,33 @@ int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t
 int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows,
                     void* stream);
 
+/* ---- timing for roofline reports ------------------------------------------
+ * When enabled, every kernel launch is bracketed by a pair of HIP events on
+ * its stream and attributed to a kernel class; the draft phase and the
+ * verify phase of each lede_step are bracketed as well.  Reading
+ * synchronises, converts the event pairs to milliseconds and (reset != 0)
+ * clears the totals.  bytes is the algorithmic HBM traffic of the launches:
+ * weights and KV read once, plus activations in and out. */
+enum {
+  LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel (draft path) */
+  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel (verify / prefill path) */
+  LEDE_K_ATTENTION,       /* paged attention partial + combine */
+  LEDE_K_NORM,            /* RMSNorm rows */
+  LEDE_K_QNET,            /* Q-network layers */
+  LEDE_K_ACCEPT,          /* acceptance scan + KV truncation */
+  LEDE_K_DRAFT_PHASE,     /* all draft passes of a step */
+  LEDE_K_VERIFY_PHASE,    /* the verify pass + acceptance of a step */
+  LEDE_K_NCLASS
+};
+typedef struct {
+  double ms;
+  double bytes;
+  int64_t launches;
+} lede_prof_entry;
+
+int lede_prof_enable(lede_ctx* ctx, int32_t on);
+int lede_prof_read(lede_ctx* ctx, lede_prof_entry* out /* [LEDE_K_NCLASS] */, int32_t reset);
+
 /* ---- single-operation entry points (kernel-level tests and tooling) ----- */
 
 /* Bytes of a tiled weight matrix of N x K (dtype LEDE_DTYPE_*). */

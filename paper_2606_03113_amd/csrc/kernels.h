@@ -150,7 +150,7 @@ hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
 
-// Bytes of dynamic LDS the linear kernels use for x rows, and its limit.
+// Bytes of dynamic LDS the linear kernels use for the staged input row.
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M);
 
 }  // namespace lede

@@ -35,12 +35,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 template <int DT> struct Elem;
 template <> struct Elem<0> {
   typedef float T;
+  static constexpr int ES_ = 4;
   static __device__ __forceinline__ float load(const void* p, size_t i) { return ((const float*)p)[i]; }
   static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((float*)p)[i] = v; }
   static __device__ __forceinline__ float round(float v) { return v; }
 };
 template <> struct Elem<1> {
   typedef uint16_t T;
+  static constexpr int ES_ = 2;
   static __device__ __forceinline__ float load(const void* p, size_t i) { return bf16_to_f32(((const uint16_t*)p)[i]); }
   static __device__ __forceinline__ void store(void* p, size_t i, float v) { ((uint16_t*)p)[i] = f32_to_bf16(v); }
   static __device__ __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
@@ -62,16 +64,6 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
-}
-
-// Deterministic block sum over 256 threads.
-__device__ __forceinline__ float block_sum256(float v, float* scratch4) {
-  v = wave_sum(v);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  __syncthreads();
-  if (lane == 0) scratch4[wave] = v;
-  __syncthreads();
-  return scratch4[0] + scratch4[1] + scratch4[2] + scratch4[3];
 }
 
 // 16-byte loads.
@@ -147,73 +139,116 @@ __global__ __launch_bounds__(256) void k_repack(RepackArgs a) {
   }
 }
 
-// ---- RMSNorm rows (verify / prefill path and the Q-network's state) ---------
+// ---- RMSNorm of one row by one wavefront ------------------------------------
+//
+// Every RMSNorm of a residual row (the norm kernel and the prologue of the
+// linear kernels) runs this routine, so a row gets the same bits whichever
+// kernel normalises it: lane l sums the squares of elements 256 j + 4 l + e
+// in increasing (j, e) order with fused multiply-adds, then an xor butterfly
+// (which leaves the same value in every lane).
+
+__device__ __forceinline__ float bf16lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+// Four consecutive elements of a row: fp32 residual h, or a model-dtype row.
+template <int DT>
+__device__ __forceinline__ float4 row_load4(const float* h, const void* row, int i) {
+  if (h) return *(const float4*)(h + i);
+  if (DT == 1) {
+    const uint2 u = *(const uint2*)((const uint16_t*)row + i);
+    return make_float4(bf16lo(u.x), bf16hi(u.x), bf16lo(u.y), bf16hi(u.y));
+  }
+  return *(const float4*)((const float*)row + i);
+}
 
 template <int DT>
-__global__ __launch_bounds__(256) void k_norm(NormArgs a) {
-  __shared__ float scratch[4];
-  const int m = blockIdx.x, tid = threadIdx.x;
-  float* h = a.h + (size_t)m * a.ldh;
-  if (m == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
-  const int tok = a.embed ? min((unsigned)a.tok.get(m), (unsigned)(a.vocab - 1)) : 0;
-  if (a.embed) {
-    for (int i = tid; i < a.d; i += 256) h[i] = Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i);
+__device__ __forceinline__ void store4(uint8_t* base, int i, float4 y) {
+  if (DT == 1) {
+    const uint32_t lo = (uint32_t)f32_to_bf16(y.x) | ((uint32_t)f32_to_bf16(y.y) << 16);
+    const uint32_t hi = (uint32_t)f32_to_bf16(y.z) | ((uint32_t)f32_to_bf16(y.w) << 16);
+    *(uint2*)(base + (size_t)i * 2) = make_uint2(lo, hi);
+  } else {
+    *(float4*)(base + (size_t)i * 4) = y;
   }
+}
+
+template <int DT>
+__device__ float wave_row_inv_rms(const float* h, const void* row, int d, float eps) {
+  const int lane = threadIdx.x & 63;
   float ss = 0.f;
-  for (int i = tid; i < a.d; i += 256) {
-    const float v = a.embed ? Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i) : h[i];
-    ss += v * v;
+  for (int j0 = 0; j0 < d; j0 += 2048) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = j0 + 256 * u + 4 * lane;
+      v[u] = i < d ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      ss = fmaf(v[u].x, v[u].x, ss);
+      ss = fmaf(v[u].y, v[u].y, ss);
+      ss = fmaf(v[u].z, v[u].z, ss);
+      ss = fmaf(v[u].w, v[u].w, ss);
+    }
   }
-  ss = block_sum256(ss, scratch);
-  const float inv = rsqrtf(ss / (float)a.d + a.eps);
-  for (int i = tid; i < a.d; i += 256) {
-    const float v = a.embed ? Elem<DT>::load(a.embed_w, (size_t)tok * a.d + i) : h[i];
-    const float y = v * inv * Elem<DT>::load(a.gain, i);
-    if (a.f32_out) ((float*)a.x)[(size_t)m * a.ldx + i] = y;
-    else Elem<DT>::store(a.x, (size_t)m * a.ldx + i, y);
+  ss = wave_sum(ss);
+  return rsqrtf(ss / (float)d + eps);
+}
+
+// Second pass: y = (x * inv) * gain for every 4-element group, written by
+// `out` (model dtype, or fp32 when OUT_F32); h_out (nullable) receives x.
+template <int DT, bool OUT_F32>
+__device__ void wave_row_normalize(const float* h, const void* row, const void* gain, int d, float inv,
+                                   float* h_out, uint8_t* out) {
+  const int lane = threadIdx.x & 63;
+  for (int j0 = 0; j0 < d; j0 += 2048) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = j0 + 256 * u + 4 * lane;
+      v[u] = i < d ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = j0 + 256 * u + 4 * lane;
+      if (i < d) {
+        const float4 g = row_load4<DT>(nullptr, gain, i);
+        float4 y;
+        y.x = (v[u].x * inv) * g.x;
+        y.y = (v[u].y * inv) * g.y;
+        y.z = (v[u].z * inv) * g.z;
+        y.w = (v[u].w * inv) * g.w;
+        if (h_out) *(float4*)(h_out + i) = v[u];
+        if (OUT_F32) store4<0>(out, i, y);
+        else store4<DT>(out, i, y);
+      }
+    }
   }
+}
+
+// RMSNorm rows for the verify / prefill path and the Q-network's state: one
+// wavefront per row.
+template <int DT>
+__global__ __launch_bounds__(64) void k_norm(NormArgs a) {
+  const int m = blockIdx.x;
+  if (m == 0 && a.zero_keys && (int)threadIdx.x < a.n_zero_keys) a.zero_keys[threadIdx.x] = 0;
+  float* h = a.h + (size_t)m * a.ldh;
+  const float* src = h;
+  const void* row = nullptr;
+  if (a.embed) {
+    // a token outside the vocabulary can only come from a fault upstream;
+    // clamping keeps the read inside the table
+    const int tok = (int)min((unsigned)a.tok.get(m), (unsigned)(a.vocab - 1));
+    row = (const uint8_t*)a.embed_w + (size_t)tok * a.d * Elem<DT>::ES_;
+    src = nullptr;
+  }
+  const float inv = wave_row_inv_rms<DT>(src, row, a.d, a.eps);
+  uint8_t* out = (uint8_t*)a.x + (size_t)m * a.ldx * (a.f32_out ? 4 : Elem<DT>::ES_);
+  if (a.f32_out) wave_row_normalize<DT, true>(src, row, a.gain, a.d, inv, a.embed ? h : nullptr, out);
+  else wave_row_normalize<DT, false>(src, row, a.gain, a.d, inv, a.embed ? h : nullptr, out);
 }
 
 // ---- linear: y = W x with fused prologue / epilogue --------------------------
-
-// Stage the (single) input row of the vector path in LDS, in the model dtype
-// (fp32 for X_F32), zero-padded to KT * TK elements.
-template <int DT>
-__device__ void stage_x_row(const LinearArgs& a, uint8_t* smem) {
-  typedef Tile<DT> TL;
-  __shared__ float scratch[4];
-  const int tid = threadIdx.x;
-  const int KP = a.KT * TL::TK;
-  if (a.x_mode == X_PLAIN || a.x_mode == X_F32) {
-    for (int i = tid; i < KP; i += 256) {
-      float v = 0.f;
-      if (i < a.K) v = (a.x_mode == X_F32) ? ((const float*)a.x)[i] : Elem<DT>::load(a.x, i);
-      Elem<DT>::store(smem, i, v);
-    }
-  } else {
-    const bool emb = a.x_mode == X_EMBED_NORM;
-    // a token outside the vocabulary can only come from a fault upstream;
-    // clamping keeps the embedding read inside its table
-    const int tok = emb ? (int)min((unsigned)a.tok.get(0), (unsigned)(a.vocab - 1)) : 0;
-    float ss = 0.f;
-    for (int i = tid; i < a.K; i += 256) {
-      const float v = emb ? Elem<DT>::load(a.embed, (size_t)tok * a.K + i) : a.h[i];
-      ss += v * v;
-      if (emb && blockIdx.x == 0) a.h[i] = v;
-    }
-    ss = block_sum256(ss, scratch);
-    const float inv = rsqrtf(ss / (float)a.K + a.eps);
-    for (int i = tid; i < KP; i += 256) {
-      float y = 0.f;
-      if (i < a.K) {
-        const float v = emb ? Elem<DT>::load(a.embed, (size_t)tok * a.K + i) : a.h[i];
-        y = v * inv * Elem<DT>::load(a.gain, i);
-      }
-      Elem<DT>::store(smem, i, y);
-    }
-  }
-  __syncthreads();
-}
 
 template <int DT>
 __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best) {
@@ -307,75 +342,170 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
   }
 }
 
-template <int DT, bool MFMA>
-__global__ __launch_bounds__(256) void k_linear(LinearArgs a) {
+// Weights are streamed once per pass: non-temporal loads keep them from
+// displacing the activations and KV pages in the caches.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld16_stream(const void* p) {
+  return __builtin_bit_cast(uint4, __builtin_nontemporal_load((const u32x4*)p));
+}
+
+// Deterministic sum over the NW wavefronts of a block (every thread takes
+// part in the barriers).
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* scratch) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  float s = scratch[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) s += scratch[w];
+  return s;
+}
+
+// Normalise the single input row of the vector kernel into LDS with every
+// thread of the block (thread t holds elements 4t + 4 NT j in registers).
+template <int DT, int NW>
+__device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch) {
+  constexpr int NT = NW * 64;
+  const int tid = threadIdx.x;
+  const float* h = a.h;
+  const void* row = nullptr;
+  float* h_out = nullptr;
+  if (a.x_mode == X_EMBED_NORM) {
+    const int tok = (int)min((unsigned)a.tok.get(0), (unsigned)(a.vocab - 1));
+    row = (const uint8_t*)a.embed + (size_t)tok * a.K * Elem<DT>::ES_;
+    if (blockIdx.x == 0) h_out = a.h;
+    h = nullptr;
+  }
+  float4 v[8];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    v[j] = i < a.K ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    ss = fmaf(v[j].x, v[j].x, ss);
+    ss = fmaf(v[j].y, v[j].y, ss);
+    ss = fmaf(v[j].z, v[j].z, ss);
+    ss = fmaf(v[j].w, v[j].w, ss);
+  }
+  ss = block_sum<NW>(ss, scratch);
+  const float inv = rsqrtf(ss / (float)a.K + a.eps);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    if (i < a.K) {
+      const float4 g = row_load4<DT>(nullptr, a.gain, i);
+      float4 y;
+      y.x = (v[j].x * inv) * g.x;
+      y.y = (v[j].y * inv) * g.y;
+      y.z = (v[j].z * inv) * g.z;
+      y.w = (v[j].w * inv) * g.w;
+      if (h_out) *(float4*)(h_out + i) = v[j];
+      store4<DT>(lds, i, y);
+    }
+  }
+  __syncthreads();
+}
+
+// y = W x over 16-row groups, one group per block.  NW waves split K (wave w
+// takes tiles w, w + NW, ...) and the partials are summed in wave order.
+// Vector kernel: one input row, dot2 instructions, the input row normalised
+// in the prologue (X_NORM / X_EMBED_NORM) or read from global memory.
+// Matrix kernel: up to 16 rows read from global memory (normalised by the
+// norm kernel), 16x16 matrix-core tiles.
+template <int DT, bool MFMA, int NW>
+__global__ __launch_bounds__(NW * 64) void k_linear(LinearArgs a) {
   typedef Tile<DT> TL;
+  constexpr int U = NW >= 8 ? 4 : 8;  // tiles per wave per batch
   extern __shared__ __align__(16) uint8_t smem[];
-  __shared__ float red[4][16][16];
+  __shared__ float red[NW][16][16];
   __shared__ float ct[16][17];
+  __shared__ float scratch[NW];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int KT = a.KT, NG = a.n_groups;
+  const bool staged = !MFMA && (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM);
+  const uint4 zero = {0u, 0u, 0u, 0u};
 
   if (blockIdx.x == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
-  if (!MFMA) stage_x_row<DT>(a, smem);
+
+  int g = blockIdx.x;
+  // the weights do not depend on the input: the first batch is in flight
+  // while the prologue normalises the input row
+  uint4 w[U];
+  {
+    const uint8_t* wg = a.w + (size_t)(g < NG ? g : 0) * KT * TILE_BYTES + lane * 16;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = wave + NW * u;
+      w[u] = (g < NG && t < KT) ? ld16_stream(wg + (size_t)t * TILE_BYTES) : zero;
+    }
+  }
+  if (staged) stage_norm_row<DT, NW>(a, smem, scratch);
 
   uint64_t best = 0;
-  const int KT = a.KT;
-  for (int g = blockIdx.x; g < a.n_groups; g += gridDim.x) {
+  bool first = true;
+  for (; g < NG; g += gridDim.x, first = false) {
     const uint8_t* wg = a.w + (size_t)g * KT * TILE_BYTES + lane * 16;
-    if (!MFMA) {
-      const uint8_t* xs = smem + (lane >> 4) * 16;
-      float acc0 = 0.f, acc1 = 0.f;
-      int t = wave;
-      for (; t + 28 < KT; t += 32) {
-        uint4 w[8], x[8];
+    const int m = MFMA ? (lane & 15) : 0;
+    const bool has = m < (MFMA ? a.M : 1);
+    const uint8_t* xb = staged ? smem + (size_t)(lane >> 4) * 16
+                               : (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
+    float acc0 = 0.f, acc1 = 0.f;
+    f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+    for (int t = wave; t < KT; t += NW * U) {
+      uint4 x[U];
+      if (!(first && t == wave)) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) w[u] = ld16(wg + (size_t)(t + 4 * u) * TILE_BYTES);
+        for (int u = 0; u < U; ++u) {
+          const int tt = t + NW * u;
+          w[u] = tt < KT ? ld16_stream(wg + (size_t)tt * TILE_BYTES) : zero;
+        }
+      }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = ld16(xs + (t + 4 * u) * 64);
+      for (int u = 0; u < U; ++u) {
+        const int tt = t + NW * u;
+        x[u] = (has && tt < KT) ? ld16(xb + (size_t)tt * TL::TK * TL::ES) : zero;
+      }
+      if (MFMA) {
 #pragma unroll
-        for (int u = 0; u < 8; u += 2) {
+        for (int u = 0; u < U; u += 2) {
+          c0 = mfma_tile<DT>(w[u], x[u], c0);
+          c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; u += 2) {
           acc0 = dot16<DT>(w[u], x[u], acc0);
           acc1 = dot16<DT>(w[u + 1], x[u + 1], acc1);
         }
       }
-      for (; t < KT; t += 4) acc0 = dot16<DT>(ld16(wg + (size_t)t * TILE_BYTES), ld16(xs + t * 64), acc0);
+    }
+    if (MFMA) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = c0[i] + c1[i];
+    } else {
       float acc = acc0 + acc1;
       acc += __shfl_xor(acc, 16);
       acc += __shfl_xor(acc, 32);
       if (lane < 16) red[wave][lane][0] = acc;
-    } else {
-      const int m = lane & 15;
-      const bool has = m < a.M;
-      const uint8_t* xr = (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
-      f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
-      const uint4 zero = {0u, 0u, 0u, 0u};
-      int t = wave;
-      for (; t + 28 < KT; t += 32) {
-        uint4 w[8], x[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) w[u] = ld16(wg + (size_t)(t + 4 * u) * TILE_BYTES);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = has ? ld16(xr + (size_t)(t + 4 * u) * TL::TK * TL::ES) : zero;
-#pragma unroll
-        for (int u = 0; u < 8; u += 2) {
-          c0 = mfma_tile<DT>(w[u], x[u], c0);
-          c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
-        }
-      }
-      for (; t < KT; t += 4) {
-        const uint4 xv = has ? ld16(xr + (size_t)t * TL::TK * TL::ES) : zero;
-        c0 = mfma_tile<DT>(ld16(wg + (size_t)t * TILE_BYTES), xv, c0);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = c0[i] + c1[i];
     }
     __syncthreads();
-    {
-      const int n = tid >> 4, m = tid & 15;
-      if (MFMA || m == 0) ct[n][m] = ((red[0][n][m] + red[1][n][m]) + red[2][n][m]) + red[3][n][m];
+    if (tid < 256) {
+      const int n = tid >> 4, mm = tid & 15;
+      if (MFMA || mm == 0) {
+        float s = red[0][n][mm];
+#pragma unroll
+        for (int q = 1; q < NW; ++q) s += red[q][n][mm];
+        ct[n][mm] = s;
+      }
     }
     __syncthreads();
-    epilogue<DT>(a, g, ct, best);
+    if (tid < 256) epilogue<DT>(a, g, ct, best);
     __syncthreads();
   }
   if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
@@ -384,13 +514,28 @@ __global__ __launch_bounds__(256) void k_linear(LinearArgs a) {
 
 // ---- attention over the paged KV cache --------------------------------------
 
+// Eight consecutive cache elements as fp32.
+template <int DT>
+__device__ __forceinline__ void load8(const void* base, size_t idx, float* o) {
+  if (DT == 1) {
+    const uint4 u = ld16((const uint16_t*)base + idx);
+    o[0] = bf16lo(u.x); o[1] = bf16hi(u.x); o[2] = bf16lo(u.y); o[3] = bf16hi(u.y);
+    o[4] = bf16lo(u.z); o[5] = bf16hi(u.z); o[6] = bf16lo(u.w); o[7] = bf16hi(u.w);
+  } else {
+    const float4 a = *(const float4*)((const float*)base + idx);
+    const float4 b = *(const float4*)((const float*)base + idx + 4);
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w; o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+}
+
 // Partial attention of up to 16 query rows (row = (m, query head of the
 // group)) against whole 64-token pages; pages are strided over the blocks of
 // a split.  For every (row, page): running max, sum of exp and the
-// exp-weighted value sum, stored for the combine kernel.
+// exp-weighted value sum, stored for the combine kernel.  A row's partials
+// do not depend on which other rows share the block.
 template <int DT, int HD>
 __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
-  constexpr int NP = 4, DPP = HD / NP, NPC = DPP / 8;  // score parts, dims per part, 8-pieces
+  constexpr int NPC = HD / 32;  // 8-element pieces per thread in the score phase
   constexpr int PV_DG = HD / 8, PV_TG = 256 / PV_DG, TPT = 64 / PV_TG;
   __shared__ float qs[16][HD];
   __shared__ float ss[16][64];
@@ -406,12 +551,17 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int pos0 = *a.seq_len + a.pos_off;
   const int pmax = pos0 + a.M - 1;
   const int n_chunks = pmax / 64 + 1;
+  if ((int)blockIdx.y >= n_chunks) return;
   const float scale = rsqrtf((float)HD);
 
-  for (int idx = tid; idx < nr * HD; idx += 256) {
-    const int r = idx / HD, i = idx % HD;
+  for (int idx = tid; idx < nr * (HD / 4); idx += 256) {
+    const int r = idx / (HD / 4), i = 4 * (idx % (HD / 4));
     const int rr = r0 + r, m = rr / G, head = kvh * G + rr % G;
-    qs[r][i] = a.q[(size_t)m * a.ldq + head * HD + i] * scale;
+    const float4 v = *(const float4*)(a.q + (size_t)m * a.ldq + head * HD + i);
+    qs[r][i] = v.x * scale;
+    qs[r][i + 1] = v.y * scale;
+    qs[r][i + 2] = v.z * scale;
+    qs[r][i + 3] = v.w * scale;
   }
   __syncthreads();
 
@@ -420,17 +570,15 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
     const int tok0 = j * 64;
     const int nvalid = min(64, pmax - tok0 + 1);
-    {  // scores
+    {  // scores: thread (token t, part p) covers dims p*8 + 32c + e
       const int t = tid >> 2, p = tid & 3;
-      float kf[DPP];
+      float kf[NPC * 8];
       if (t < nvalid) {
 #pragma unroll
-        for (int c = 0; c < NPC; ++c)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) kf[8 * c + e] = Elem<DT>::load(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c + e);
+        for (int c = 0; c < NPC; ++c) load8<DT>(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c, kf + 8 * c);
       } else {
 #pragma unroll
-        for (int e = 0; e < DPP; ++e) kf[e] = 0.f;
+        for (int e = 0; e < NPC * 8; ++e) kf[e] = 0.f;
       }
       for (int r = 0; r < nr; ++r) {
         float s = 0.f;
@@ -457,15 +605,16 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       }
     }
     __syncthreads();
-    {  // exp-weighted values
+    {  // exp-weighted values: thread (dim group dg, token group tg)
       const int dg = tid % PV_DG, tg = tid / PV_DG;
       float vf[TPT][8];
 #pragma unroll
       for (int u = 0; u < TPT; ++u) {
         const int t = tg + PV_TG * u;
+        if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
+        else
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          vf[u][e] = (t < nvalid) ? Elem<DT>::load(a.vcache, base + (size_t)t * HD + dg * 8 + e) : 0.f;
+          for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
       }
       for (int r = 0; r < nr; ++r) {
         float o[8];
@@ -509,42 +658,56 @@ __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
   const int nc = pos / 64 + 1;
   const float* p = a.part + ((size_t)m * a.nq + head) * a.max_chunks * (HD + 2);
   float mx = -INFINITY, l = 0.f, acc = 0.f;
-  for (int j = 0; j < nc; ++j, p += HD + 2) {
-    const float pm = p[0], pl = p[1], pa = p[2 + i];
-    const float nm = fmaxf(mx, pm);
-    const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
-    const float sn = __expf(pm - nm);
-    l = l * so + pl * sn;
-    acc = acc * so + pa * sn;
-    mx = nm;
+  for (int j0 = 0; j0 < nc; j0 += 8) {
+    float pm[8], pl[8], pa[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* q = p + (size_t)(j0 + u) * (HD + 2);
+      const bool ok = j0 + u < nc;
+      pm[u] = ok ? q[0] : -INFINITY;
+      pl[u] = ok ? q[1] : 0.f;
+      pa[u] = ok ? q[2 + i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (j0 + u >= nc) break;
+      const float nm = fmaxf(mx, pm[u]);
+      const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
+      const float sn = __expf(pm[u] - nm);
+      l = l * so + pl[u] * sn;
+      acc = acc * so + pa[u] * sn;
+      mx = nm;
+    }
   }
   Elem<DT>::store(a.out, (size_t)m * a.ldo + head * HD + i, acc / l);
 }
 
 // ---- Q-network output layer + argmax ----------------------------------------
 
+// One wavefront per action: q[j] = sum_i W2[j][i] hid[i] + b2[j]; argmax with
+// the lowest index on ties.
 __global__ __launch_bounds__(256) void k_qnet_out(QnetOutArgs a) {
-  __shared__ unsigned long long best[256];
-  const int tid = threadIdx.x;
+  __shared__ unsigned long long best[4];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   uint64_t b = 0;
-  for (int j = tid; j < a.A; j += 256) {
+  for (int j = wave; j < a.A; j += 4) {
     float s = 0.f;
-    for (int i = 0; i < a.H; ++i) s = fmaf(a.w2[(size_t)j * a.H + i], a.hid[i], s);
-    s += a.b2[j];
-    a.qv[j] = s;
+    for (int i = lane; i < a.H; i += 64) s = fmaf(a.w2[(size_t)j * a.H + i], a.hid[i], s);
+    s = wave_sum(s) + a.b2[j];
+    if (lane == 0) a.qv[j] = s;
     const uint64_t key = argmax_key(s, j);
     b = key > b ? key : b;
   }
-  best[tid] = b;
+  if (lane == 0) best[wave] = b;
   __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if (tid < o) best[tid] = best[tid + o] > best[tid] ? best[tid + o] : best[tid];
-    __syncthreads();
-  }
   if (tid == 0) {
-    const int idx = (int)(0xFFFFFFFFu - (uint32_t)(best[0] & 0xFFFFFFFFull));
+    uint64_t m = best[0];
+    for (int w = 1; w < 4; ++w) m = best[w] > m ? best[w] : m;
+    const int idx = (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull));
     a.action[0] = idx;
-    a.action[1] = __float_as_int(a.qv[idx]);
+    uint32_t u = (uint32_t)(m >> 32);
+    u = (u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u;  // undo the key's ordering transform
+    a.action[1] = (int)u;
   }
 }
 
@@ -593,27 +756,33 @@ hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s) {
-  if (dtype == 1) hipLaunchKernelGGL(k_norm<1>, dim3(a.M), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(k_norm<0>, dim3(a.M), dim3(256), 0, s, a);
+  if (dtype == 1) hipLaunchKernelGGL(k_norm<1>, dim3(a.M), dim3(64), 0, s, a);
+  else hipLaunchKernelGGL(k_norm<0>, dim3(a.M), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
   (void)M;
-  if (mfma) return 0;
-  const int tk = tile_k(dtype);
-  const int kp = ((K + tk - 1) / tk) * tk;
-  return (size_t)kp * (dtype == 1 ? 2 : 4);
+  if (mfma || (x_mode != X_NORM && x_mode != X_EMBED_NORM)) return 0;
+  return (size_t)K * (dtype == 1 ? 2 : 4);
+}
+
+int linear_waves(int n_groups) { return n_groups >= 512 ? 4 : 8; }
+
+template <int DT, bool MFMA>
+static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s) {
+  if (linear_waves(a.n_groups) == 4) hipLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), lds, s, a);
+  else hipLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), lds, s, a);
 }
 
 hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s) {
   const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
   if (dtype == 1) {
-    if (mfma) hipLaunchKernelGGL((k_linear<1, true>), dim3(grid), dim3(256), lds, s, a);
-    else hipLaunchKernelGGL((k_linear<1, false>), dim3(grid), dim3(256), lds, s, a);
+    if (mfma) launch_linear_t<1, true>(a, grid, lds, s);
+    else launch_linear_t<1, false>(a, grid, lds, s);
   } else {
-    if (mfma) hipLaunchKernelGGL((k_linear<0, true>), dim3(grid), dim3(256), lds, s, a);
-    else hipLaunchKernelGGL((k_linear<0, false>), dim3(grid), dim3(256), lds, s, a);
+    if (mfma) launch_linear_t<0, true>(a, grid, lds, s);
+    else launch_linear_t<0, false>(a, grid, lds, s);
   }
   return hipGetLastError();
 }

@@ -143,6 +143,15 @@ struct lede_ctx {
   int last_rows = 0, last_draft_rows = 0;
   std::string err;
 
+  // timing (lede_prof_*): event pairs per launch, folded into per-class totals
+  struct ProfRec { int cls; hipEvent_t a, b; double bytes; };
+  bool prof = false;
+  std::vector<hipEvent_t> evpool;
+  size_t ev_next = 0;
+  std::vector<ProfRec> recs;
+  double p_ms[LEDE_K_NCLASS] = {0}, p_bytes[LEDE_K_NCLASS] = {0};
+  int64_t p_n[LEDE_K_NCLASS] = {0};
+
   // device pointers
   template <typename T> T* W(size_t off) const { return (T*)(w + off); }
   template <typename T> T* S(size_t off) const { return (T*)(ws + off); }
@@ -169,6 +178,77 @@ int fail(lede_ctx* c, int code, const char* fmt, ...) {
   } while (0)
 
 hipStream_t S_(void* s) { return (hipStream_t)s; }
+
+// ---- timing ------------------------------------------------------------------------
+
+hipEvent_t next_event(lede_ctx* c) {
+  if (c->ev_next == c->evpool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    c->evpool.push_back(e);
+  }
+  return c->evpool[c->ev_next++];
+}
+
+int prof_mark(lede_ctx* c, hipStream_t s, hipEvent_t* e) {
+  *e = nullptr;
+  if (!c->prof) return LEDE_OK;
+  *e = next_event(c);
+  if (!*e) return fail(c, LEDE_E_HIP, "hipEventCreate failed");
+  HIP_CHECK(c, hipEventRecord(*e, s));
+  return LEDE_OK;
+}
+
+int prof_close(lede_ctx* c, hipStream_t s, int cls, double bytes, hipEvent_t e0) {
+  if (!c->prof || !e0) return LEDE_OK;
+  hipEvent_t e1 = nullptr;
+  int rc = prof_mark(c, s, &e1);
+  if (rc) return rc;
+  c->recs.push_back({cls, e0, e1, bytes});
+  return LEDE_OK;
+}
+
+// Convert finished event pairs into per-class totals (synchronises).
+int prof_fold(lede_ctx* c) {
+  if (c->recs.empty()) { c->ev_next = 0; return LEDE_OK; }
+  HIP_CHECK(c, hipEventSynchronize(c->recs.back().b));
+  for (const auto& r : c->recs) {
+    float ms = 0.f;
+    HIP_CHECK(c, hipEventElapsedTime(&ms, r.a, r.b));
+    c->p_ms[r.cls] += ms;
+    c->p_bytes[r.cls] += r.bytes;
+    c->p_n[r.cls] += 1;
+  }
+  c->recs.clear();
+  c->ev_next = 0;
+  return LEDE_OK;
+}
+
+#define LAUNCH(cls, bytes, expr)                         \
+  do {                                                   \
+    hipEvent_t e0_ = nullptr;                            \
+    int rc_ = prof_mark(c, s, &e0_);                     \
+    if (rc_) return rc_;                                 \
+    HIP_CHECK(c, (expr));                                \
+    rc_ = prof_close(c, s, (cls), (bytes), e0_);         \
+    if (rc_) return rc_;                                 \
+  } while (0)
+
+// Algorithmic bytes of one linear launch: weights once, input rows, outputs.
+double linear_bytes(const LinearArgs& a, int dt) {
+  const double es = dt == 1 ? 2.0 : 4.0;
+  const double N = (double)a.n_groups * 16, K = a.K, M = a.M;
+  double x = (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM || a.x_mode == X_F32) ? M * K * 4 : M * K * es;
+  double y = 0;
+  switch (a.epi) {
+    case EPI_RESID: y = 2 * M * N * 4; break;
+    case EPI_QKV: y = M * N * 4; break;
+    case EPI_SWIGLU: y = M * N / 2 * es; break;
+    case EPI_ARGMAX: y = M * 8 + (a.logits ? M * N * 4 : 0); break;
+    default: y = M * N * 4;
+  }
+  return N * K * es + x + y;
+}
 
 // ---- page allocator (host) ------------------------------------------------------
 
@@ -207,8 +287,18 @@ int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
 // ---- pass orchestration -----------------------------------------------------------
 
 int linear_grid(int n_groups, int epi) {
-  const int cap = epi == EPI_ARGMAX ? 1024 : 4096;
-  return std::min(n_groups, cap);
+  // one 16-row group per block; the argmax head caps the block count to
+  // bound its atomic updates
+  return epi == EPI_ARGMAX ? std::min(n_groups, 1024) : n_groups;
+}
+
+// The verify / prefill rows are normalised by the norm kernel (one
+// wavefront per row) rather than in every block of the matrix-core kernel:
+// re-reading k+1 residual rows per block costs more than one launch.
+bool fuse_norm(const lede_ctx* c, int M) {
+  (void)c;
+  (void)M;
+  return false;
 }
 
 LinearArgs base_linear(const lede_ctx* c) {
@@ -244,13 +334,13 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     qa.layer = j; qa.n_pages = o.n_pages; qa.nq = o.nq; qa.nkv = o.nkv; qa.hd = o.hd;
     qa.block_table = c->S<int32_t>(o.btab); qa.seq_len = c->S<int32_t>(o.seq_len); qa.pos_off = pos_off;
     qa.rope = c->S<float2>(o.rope);
-    if (vec) {
+    if (vec || fuse_norm(c, M)) {
       qa.x_mode = first ? X_EMBED_NORM : X_NORM;
       qa.gain = c->W<void>(lw.attn_norm);
       qa.embed = c->W<void>(o.embed);
       qa.tok = tok;
       qa.vocab = o.V;
-      if (first && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = 1; }
+      if (first && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = vec ? 1 : M; }
     } else {
       NormArgs na{};
       na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
@@ -258,10 +348,11 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       na.embed = first; na.embed_w = c->W<void>(o.embed); na.tok = tok; na.vocab = o.V;
       na.x = c->S<void>(o.xn);
       if (first && zero_slot) { na.zero_keys = zero_slot; na.n_zero_keys = M; }
-      HIP_CHECK(c, launch_norm(dt, na, s));
+      LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
       qa.x_mode = X_PLAIN; qa.x = c->S<void>(o.xn); qa.ldx = o.d;
     }
-    HIP_CHECK(c, launch_linear(dt, !vec, qa, linear_grid(qa.n_groups, qa.epi), s));
+    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(qa, dt),
+           launch_linear(dt, !vec, qa, linear_grid(qa.n_groups, qa.epi), s));
 
     AttnArgs at{};
     at.q = c->S<float>(o.q); at.ldq = o.qd;
@@ -275,7 +366,9 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     at.max_chunks = o.max_chunks;
     at.part = c->S<float>(o.part);
     at.out = c->S<void>(o.attn_out); at.ldo = o.qd;
-    HIP_CHECK(c, launch_attention(dt, at, s));
+    const double n_pos = (double)c->seq_len + pos_off + M;
+    LAUNCH(LEDE_K_ATTENTION, n_pos * o.kvd * 2.0 * o.es + 2.0 * M * o.qd * 4,
+           launch_attention(dt, at, s));
 
     LinearArgs oa = base_linear(c);
     oa.M = M;
@@ -283,7 +376,8 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
     oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
     oa.epi = EPI_RESID;
-    HIP_CHECK(c, launch_linear(dt, !vec, oa, linear_grid(oa.n_groups, oa.epi), s));
+    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(oa, dt),
+           launch_linear(dt, !vec, oa, linear_grid(oa.n_groups, oa.epi), s));
 
     // feed-forward block
     LinearArgs ga = base_linear(c);
@@ -291,17 +385,18 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     ga.w = c->W<uint8_t>(lw.wgu);
     ga.n_groups = 2 * o.F / 16; ga.KT = k_tiles(dt, o.d); ga.K = o.d;
     ga.epi = EPI_SWIGLU; ga.act = c->S<void>(o.act); ga.ld_act = o.Fp;
-    if (vec) {
+    if (vec || fuse_norm(c, M)) {
       ga.x_mode = X_NORM; ga.gain = c->W<void>(lw.ffn_norm);
     } else {
       NormArgs na{};
       na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
       na.h = c->S<float>(o.h); na.gain = c->W<void>(lw.ffn_norm); na.eps = c->cfg.rms_eps;
       na.x = c->S<void>(o.xn);
-      HIP_CHECK(c, launch_norm(dt, na, s));
+      LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
       ga.x_mode = X_PLAIN; ga.x = c->S<void>(o.xn); ga.ldx = o.d;
     }
-    HIP_CHECK(c, launch_linear(dt, !vec, ga, linear_grid(ga.n_groups, ga.epi), s));
+    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(ga, dt),
+           launch_linear(dt, !vec, ga, linear_grid(ga.n_groups, ga.epi), s));
 
     LinearArgs da = base_linear(c);
     da.M = M;
@@ -309,25 +404,26 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
     da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
     da.epi = EPI_RESID;
-    HIP_CHECK(c, launch_linear(dt, !vec, da, linear_grid(da.n_groups, da.epi), s));
+    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(da, dt),
+           launch_linear(dt, !vec, da, linear_grid(da.n_groups, da.epi), s));
 
     if (qnet_after == j + 1 && o.H > 0) {
       NormArgs na{};
       na.M = 1; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
       na.h = c->S<float>(o.h); na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
       na.x = c->S<void>(o.qs); na.f32_out = 1;
-      HIP_CHECK(c, launch_norm(dt, na, s));
+      LAUNCH(LEDE_K_QNET, (double)o.d * 8, launch_norm(dt, na, s));
       LinearArgs la = base_linear(c);
       la.w = c->W<uint8_t>(o.qw1);
       la.n_groups = o.H / 16; la.KT = k_tiles(0, o.d); la.K = o.d;
       la.x_mode = X_F32; la.x = c->S<void>(o.qs);
       la.epi = EPI_BIAS_RELU; la.out = c->S<float>(o.qhid); la.bias = c->W<float>(o.qb1);
-      HIP_CHECK(c, launch_linear(0, false, la, la.n_groups, s));
+      LAUNCH(LEDE_K_QNET, linear_bytes(la, 0), launch_linear(0, false, la, la.n_groups, s));
       QnetOutArgs qo{};
       qo.hid = c->S<float>(o.qhid); qo.H = o.H;
       qo.w2 = c->W<float>(o.qw2); qo.b2 = c->W<float>(o.qb2); qo.A = o.A;
       qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.qaction);
-      HIP_CHECK(c, launch_qnet_out(qo, s));
+      LAUNCH(LEDE_K_QNET, (double)o.A * (o.H + 2) * 4, launch_qnet_out(qo, s));
     }
   }
   return LEDE_OK;
@@ -342,17 +438,18 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
   ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
   ha.logits = logits; ha.ld_logits = o.V;
-  if (vec) {
+  if (vec || fuse_norm(c, M)) {
     ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
   } else {
     NormArgs na{};
     na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
     na.h = c->S<float>(o.h); na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
     na.x = c->S<void>(o.xn);
-    HIP_CHECK(c, launch_norm(o.dt, na, s));
+    LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(o.dt, na, s));
     ha.x_mode = X_PLAIN; ha.x = c->S<void>(o.xn); ha.ldx = o.d;
   }
-  HIP_CHECK(c, launch_linear(o.dt, !vec, ha, linear_grid(ha.n_groups, ha.epi), s));
+  LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(ha, o.dt),
+         launch_linear(o.dt, !vec, ha, linear_grid(ha.n_groups, ha.epi), s));
   return LEDE_OK;
 }
 
@@ -391,7 +488,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s) {
   aa.block_table = c->S<int32_t>(c->lo.btab);
   aa.pending_out = dk;
   aa.record = c->S<int32_t>(c->lo.record);
-  HIP_CHECK(c, launch_accept(aa, s));
+  LAUNCH(LEDE_K_ACCEPT, 256.0, launch_accept(aa, s));
   c->last_rows = k + 1;
   return LEDE_OK;
 }
@@ -475,6 +572,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
 
 void lede_destroy(lede_ctx* c) {
   if (!c) return;
+  for (hipEvent_t e : c->evpool) (void)hipEventDestroy(e);
   if (c->table_h) (void)hipHostFree(c->table_h);
   if (c->record_h) (void)hipHostFree(c->record_h);
   if (c->keys_h) (void)hipHostFree(c->keys_h);
@@ -669,6 +767,7 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   const Layout& o = c->lo;
   if (!forced && !o.H) return fail(c, LEDE_E_STATE, "no Q-network configured");
   hipStream_t s = S_(stream);
+  int rc0 = 0;
   memset(rec, 0, sizeof *rec);
   rec->q_action = -1;
   const int c0 = c->seq_len;
@@ -679,9 +778,12 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   }
   const int l_min = o.H ? c->cfg.exits[0] : 0;
   const bool want_q = o.H && (!forced || log_qnet);
+  hipEvent_t ph0 = nullptr;
+  if ((rc0 = prof_mark(c, s, &ph0))) return rc0;
   int k_eff = forced ? std::min(k, n_remaining - 1) : std::min(o.k_max, n_remaining - 1);
   bool ran_q = false;
   int rc;
+  (void)rc0;
   if (k_eff > 0) {
     if (!forced) {
       // the agent decides at the first candidate layer of the first draft's
@@ -712,12 +814,17 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
     k_eff = 0;
     if ((rc = ensure_pages(c, c0 + 1)) || (rc = upload_table(c, s))) return rc;
   }
+  if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
+  hipEvent_t ph1 = nullptr;
+  if ((rc = prof_mark(c, s, &ph1))) return rc;
   rc = launch_verify(c, k_eff, s);
   if (rc) return rc;
+  if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
   if (ran_q) HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
   rc = read_record(c, s);
   if (rc) return rc;
   commit_host(c);
+  if ((rc = prof_fold(c))) return rc;
   const int a = c->record_h[0];
   rec->l = l;
   rec->k_req = k;
@@ -774,6 +881,27 @@ int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t
   HIP_CHECK(c, hipMemcpyAsync(host, src, n * 4, hipMemcpyDeviceToHost, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
   if (rows) *rows = r;
+  return LEDE_OK;
+}
+
+int lede_prof_enable(lede_ctx* c, int32_t on) {
+  if (!c) return LEDE_E_ARG;
+  int rc = prof_fold(c);
+  if (rc) return rc;
+  c->prof = on != 0;
+  return LEDE_OK;
+}
+
+int lede_prof_read(lede_ctx* c, lede_prof_entry* out, int32_t reset) {
+  if (!c || !out) return fail(c, LEDE_E_ARG, "null argument");
+  int rc = prof_fold(c);
+  if (rc) return rc;
+  for (int i = 0; i < LEDE_K_NCLASS; ++i) {
+    out[i].ms = c->p_ms[i];
+    out[i].bytes = c->p_bytes[i];
+    out[i].launches = c->p_n[i];
+    if (reset) c->p_ms[i] = c->p_bytes[i] = 0, c->p_n[i] = 0;
+  }
   return LEDE_OK;
 }
 

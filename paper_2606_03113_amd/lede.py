@@ -38,6 +38,15 @@ class LedeConfig(ctypes.Structure):
                 ("k_max", ctypes.c_int32)]
 
 
+class LedeProfEntry(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double), ("bytes", ctypes.c_double), ("launches", ctypes.c_int64)]
+
+
+K_LINEAR_VEC, K_LINEAR_MFMA, K_ATTENTION, K_NORM, K_QNET, K_ACCEPT, K_DRAFT_PHASE, K_VERIFY_PHASE = range(8)
+K_NCLASS = 8
+K_NAMES = ["linear_vec", "linear_mfma", "attention", "norm", "qnet", "accept", "draft_phase", "verify_phase"]
+
+
 class LedeAction(ctypes.Structure):
     _fields_ = [("l", ctypes.c_int32), ("k", ctypes.c_int32)]
 
@@ -52,7 +61,7 @@ class LedeStepRecord(ctypes.Structure):
 EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error", "lede_load_tensor",
             "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
-            "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear"]
+            "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear"]
 
 _lib = None
 
@@ -84,6 +93,8 @@ def load(path: str = LIB_PATH):
     L.lede_step.argtypes = [vp, P(LedeAction), i32, i32, vp, P(LedeStepRecord)]
     L.lede_get_kv_state.argtypes = [vp, P(i32), P(i32), P(i32), i32, P(i32)]
     L.lede_debug_read.argtypes = [vp, i32, P(ctypes.c_float), sz, P(i32), vp]
+    L.lede_prof_enable.argtypes = [vp, i32]
+    L.lede_prof_read.argtypes = [vp, P(LedeProfEntry), i32]
     L.lede_op_tiled_bytes.argtypes = [i32, i32, i32]
     L.lede_op_tiled_bytes.restype = sz
     L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
@@ -265,6 +276,15 @@ class Engine:
         self._check(self.L.lede_debug_read(self.ctx, which, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
                                            n_floats, ctypes.byref(rows), self.stream), self.ctx)
         return out, rows.value
+
+    def lede_prof_enable(self, on: bool):
+        self._check(self.L.lede_prof_enable(self.ctx, int(on)), self.ctx)
+
+    def lede_prof_read(self, reset: bool = True) -> dict:
+        arr = (LedeProfEntry * K_NCLASS)()
+        self._check(self.L.lede_prof_read(self.ctx, arr, int(reset)), self.ctx)
+        return {K_NAMES[i]: {"ms": arr[i].ms, "bytes": arr[i].bytes, "launches": arr[i].launches}
+                for i in range(K_NCLASS)}
 
     def logits(self, which: int = 0) -> np.ndarray:
         """Debug logits of the last verify/prefill head (which=0) or of the
