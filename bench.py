@@ -53,16 +53,19 @@ def kernel_source_sha():
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(kernel_name, workload):
-    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
-    taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.json" % (kernel_name, workload))
+def traffic_from_profile(kclass, workload, launches):
+    """HBM bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE runs (profiles/traffic_*.txt), if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s_%s.txt" % (kclass, workload))
     if not os.path.exists(path):
         return None
-    d = json.load(open(path))
-    if d.get("kernel_src_sha") != kernel_source_sha():
-        return None
-    return d.get("hbm_bytes_per_launch")
+    for line in open(path):
+        if line.startswith("traffic_json:"):
+            d = json.loads(line.split(":", 1)[1])
+            if d.get("kernel_src_sha") == kernel_source_sha():
+                return d.get("hbm_bytes_per_launch")
+    return None
 
 
 def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
@@ -106,10 +109,13 @@ def main():
     ap.add_argument("--prof-steps", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graphs", type=int, default=0)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before timing, copy this many MiB device-to-device three times (a kernel of "
+                         "known traffic for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (see the sharding "
-              "design notes); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the decode path runs on a single device and has no "
+              "multi-GPU mode; run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -137,6 +143,16 @@ def main():
     log("weights resident (%.1f GB arena)  %.1f s" % (eng.region_bytes[0] / 1e9, time.time() - t0))
     first = eng.lede_prefill(prompt)
     log("prefill %d tokens done  %.1f s" % (wl.prompt_len, time.time() - t0))
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("calibration copies of %d MiB done" % args.calib_copy_mib)
 
     produced = [first]
     log_q = m.qnet_hidden > 0
@@ -178,12 +194,13 @@ def main():
     prof_recs = [step() for _ in range(args.prof_steps)]
     prof = eng.lede_prof_read(reset=True)
     eng.lede_prof_enable(False)
-    lin = {n: prof[n] for n in ("linear_vec", "linear_mfma")}
+    from paper_2606_03113_amd.lede import K_SYMBOLS
+    lin = {n: prof[n] for n in K_SYMBOLS}
     dom = max(lin, key=lambda n: lin[n]["ms"])
     d = lin[dom]
     achieved = d["bytes"] / (d["ms"] * 1e6)  # GB/s
-    kname = {"linear_vec": "k_linear_bf16_vec", "linear_mfma": "k_linear_bf16_mfma"}[dom]
-    traffic = traffic_from_profile(kname, wl.name)
+    kname = K_SYMBOLS[dom]
+    traffic = traffic_from_profile(dom, wl.name, d["launches"])
     dp, vp = prof["draft_phase"], prof["verify_phase"]
     # algorithmic bytes of the instrumented steps' passes
     db = vb = 0.0

@@ -110,8 +110,8 @@ typedef struct {
 /* Bytes of the three device regions the caller allocates for `cfg`:
  * the weight arena (repacked weights), the KV pool and the workspace.
  * Returns LEDE_E_UNSUPPORTED for shapes the kernels do not handle
- * (head_dim not 64/128, d_model or q_dim not a multiple of 32, ffn_dim not
- * a multiple of 8, page_size != 64, k_max > 15, ...). */
+ * (head_dim not 64/128, d_model or q_dim not a multiple of 32, d_model above
+ * 8192, ffn_dim not a multiple of 8, page_size != 64, k_max > 15, ...). */
 int lede_region_bytes(const lede_config* cfg, size_t* weight_bytes, size_t* kv_bytes,
                       size_t* workspace_bytes);
 
@@ -201,14 +201,16 @@ int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats
  * clears the totals.  bytes is the algorithmic HBM traffic of the launches:
  * weights and KV read once, plus activations in and out. */
 enum {
-  LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel (draft path) */
-  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel (verify / prefill path) */
+  LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel, 4 wavefronts (draft path, >= 512 row groups) */
+  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel, 4 wavefronts (verify / prefill path) */
   LEDE_K_ATTENTION,       /* paged attention partial + combine */
   LEDE_K_NORM,            /* RMSNorm rows */
   LEDE_K_QNET,            /* Q-network layers */
   LEDE_K_ACCEPT,          /* acceptance scan + KV truncation */
   LEDE_K_DRAFT_PHASE,     /* all draft passes of a step */
   LEDE_K_VERIFY_PHASE,    /* the verify pass + acceptance of a step */
+  LEDE_K_LINEAR_VEC8,     /* one-row linear kernel, 8 wavefronts (< 512 row groups) */
+  LEDE_K_LINEAR_MFMA8,    /* matrix-core linear kernel, 8 wavefronts */
   LEDE_K_NCLASS
 };
 typedef struct {

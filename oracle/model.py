@@ -11,7 +11,7 @@ Section 3.3 (exit layer chosen during the first forward pass of a step, then
 drafting at that layer); Section 4.1 (batch 1, greedy decoding, speculative
 acceptance, metrics E, d, acceptance rate).
 
-Readings where the paper is silent (each is also listed in the design notes):
+Readings where the paper is silent:
 * the early-exit head is the shared final RMSNorm + LM head;
 * acceptance is greedy: the longest prefix of drafts equal to the full
   model's argmax, plus the full model's token after it (the bonus token);

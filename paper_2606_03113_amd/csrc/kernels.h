@@ -143,12 +143,17 @@ struct AcceptArgs {
 // Launchers (kernels.hip).  All return hipError_t of the launch.
 hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s);
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s);
-hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s);
+// e0 / e1 (optional): events recorded by the dispatch at kernel start / end.
+hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s,
+                         hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
+
+// Wavefronts per block of the linear kernel for a matrix of n_groups row groups.
+int linear_waves(int n_groups);
 
 // Bytes of dynamic LDS the linear kernels use for the staged input row.
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M);

@@ -13,6 +13,7 @@
 // autoregressive step.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
 #include <math.h>
 
 namespace lede {
@@ -139,13 +140,7 @@ __global__ __launch_bounds__(256) void k_repack(RepackArgs a) {
   }
 }
 
-// ---- RMSNorm of one row by one wavefront ------------------------------------
-//
-// Every RMSNorm of a residual row (the norm kernel and the prologue of the
-// linear kernels) runs this routine, so a row gets the same bits whichever
-// kernel normalises it: lane l sums the squares of elements 256 j + 4 l + e
-// in increasing (j, e) order with fused multiply-adds, then an xor butterfly
-// (which leaves the same value in every lane).
+// ---- RMSNorm ------------------------------------------------------------------
 
 __device__ __forceinline__ float bf16lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
@@ -172,66 +167,14 @@ __device__ __forceinline__ void store4(uint8_t* base, int i, float4 y) {
   }
 }
 
-template <int DT>
-__device__ float wave_row_inv_rms(const float* h, const void* row, int d, float eps) {
-  const int lane = threadIdx.x & 63;
-  float ss = 0.f;
-  for (int j0 = 0; j0 < d; j0 += 2048) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = j0 + 256 * u + 4 * lane;
-      v[u] = i < d ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      ss = fmaf(v[u].x, v[u].x, ss);
-      ss = fmaf(v[u].y, v[u].y, ss);
-      ss = fmaf(v[u].z, v[u].z, ss);
-      ss = fmaf(v[u].w, v[u].w, ss);
-    }
-  }
-  ss = wave_sum(ss);
-  return rsqrtf(ss / (float)d + eps);
-}
-
-// Second pass: y = (x * inv) * gain for every 4-element group, written by
-// `out` (model dtype, or fp32 when OUT_F32); h_out (nullable) receives x.
-template <int DT, bool OUT_F32>
-__device__ void wave_row_normalize(const float* h, const void* row, const void* gain, int d, float inv,
-                                   float* h_out, uint8_t* out) {
-  const int lane = threadIdx.x & 63;
-  for (int j0 = 0; j0 < d; j0 += 2048) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = j0 + 256 * u + 4 * lane;
-      v[u] = i < d ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int i = j0 + 256 * u + 4 * lane;
-      if (i < d) {
-        const float4 g = row_load4<DT>(nullptr, gain, i);
-        float4 y;
-        y.x = (v[u].x * inv) * g.x;
-        y.y = (v[u].y * inv) * g.y;
-        y.z = (v[u].z * inv) * g.z;
-        y.w = (v[u].w * inv) * g.w;
-        if (h_out) *(float4*)(h_out + i) = v[u];
-        if (OUT_F32) store4<0>(out, i, y);
-        else store4<DT>(out, i, y);
-      }
-    }
-  }
-}
-
 // RMSNorm rows for the verify / prefill path and the Q-network's state: one
-// wavefront per row.
+// block of 256 threads per row, every load issued before the first use
+// (thread t holds elements 4t + 1024 j in registers).
 template <int DT>
-__global__ __launch_bounds__(64) void k_norm(NormArgs a) {
-  const int m = blockIdx.x;
-  if (m == 0 && a.zero_keys && (int)threadIdx.x < a.n_zero_keys) a.zero_keys[threadIdx.x] = 0;
+__global__ __launch_bounds__(256) void k_norm(NormArgs a) {
+  __shared__ float scratch[4];
+  const int m = blockIdx.x, tid = threadIdx.x;
+  if (m == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
   float* h = a.h + (size_t)m * a.ldh;
   const float* src = h;
   const void* row = nullptr;
@@ -242,10 +185,41 @@ __global__ __launch_bounds__(64) void k_norm(NormArgs a) {
     row = (const uint8_t*)a.embed_w + (size_t)tok * a.d * Elem<DT>::ES_;
     src = nullptr;
   }
-  const float inv = wave_row_inv_rms<DT>(src, row, a.d, a.eps);
+  float4 v[8], g[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = 4 * tid + 1024 * j;
+    v[j] = i < a.d ? row_load4<DT>(src, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    g[j] = i < a.d ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    ss = fmaf(v[j].x, v[j].x, ss);
+    ss = fmaf(v[j].y, v[j].y, ss);
+    ss = fmaf(v[j].z, v[j].z, ss);
+    ss = fmaf(v[j].w, v[j].w, ss);
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) scratch[tid >> 6] = ss;
+  __syncthreads();
+  ss = ((scratch[0] + scratch[1]) + scratch[2]) + scratch[3];
+  const float inv = rsqrtf(ss / (float)a.d + a.eps);
   uint8_t* out = (uint8_t*)a.x + (size_t)m * a.ldx * (a.f32_out ? 4 : Elem<DT>::ES_);
-  if (a.f32_out) wave_row_normalize<DT, true>(src, row, a.gain, a.d, inv, a.embed ? h : nullptr, out);
-  else wave_row_normalize<DT, false>(src, row, a.gain, a.d, inv, a.embed ? h : nullptr, out);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = 4 * tid + 1024 * j;
+    if (i < a.d) {
+      float4 y;
+      y.x = (v[j].x * inv) * g[j].x;
+      y.y = (v[j].y * inv) * g[j].y;
+      y.z = (v[j].z * inv) * g[j].z;
+      y.w = (v[j].w * inv) * g[j].w;
+      if (a.embed) *(float4*)(h + i) = v[j];
+      if (a.f32_out) store4<0>(out, i, y);
+      else store4<DT>(out, i, y);
+    }
+  }
 }
 
 // ---- linear: y = W x with fused prologue / epilogue --------------------------
@@ -553,6 +527,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int n_chunks = pmax / 64 + 1;
   if ((int)blockIdx.y >= n_chunks) return;
   const float scale = rsqrtf((float)HD);
+  int page = a.block_table[blockIdx.y];  // in flight with the query loads
 
   for (int idx = tid; idx < nr * (HD / 4); idx += 256) {
     const int r = idx / (HD / 4), i = 4 * (idx % (HD / 4));
@@ -566,10 +541,20 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   __syncthreads();
 
   for (int j = blockIdx.y; j < n_chunks; j += a.n_split) {
-    const int page = a.block_table[j];
     const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
     const int tok0 = j * 64;
     const int nvalid = min(64, pmax - tok0 + 1);
+    if (j + a.n_split < n_chunks) page = a.block_table[j + a.n_split];
+    const int dg = tid % PV_DG, tg = tid / PV_DG;
+    float vf[TPT][8];  // values are loaded together with the keys
+#pragma unroll
+    for (int u = 0; u < TPT; ++u) {
+      const int t = tg + PV_TG * u;
+      if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
+      else
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
+    }
     {  // scores: thread (token t, part p) covers dims p*8 + 32c + e
       const int t = tid >> 2, p = tid & 3;
       float kf[NPC * 8];
@@ -606,16 +591,6 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
     }
     __syncthreads();
     {  // exp-weighted values: thread (dim group dg, token group tg)
-      const int dg = tid % PV_DG, tg = tid / PV_DG;
-      float vf[TPT][8];
-#pragma unroll
-      for (int u = 0; u < TPT; ++u) {
-        const int t = tg + PV_TG * u;
-        if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
-        else
-#pragma unroll
-          for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
-      }
       for (int r = 0; r < nr; ++r) {
         float o[8];
 #pragma unroll
@@ -756,8 +731,8 @@ hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s) {
-  if (dtype == 1) hipLaunchKernelGGL(k_norm<1>, dim3(a.M), dim3(64), 0, s, a);
-  else hipLaunchKernelGGL(k_norm<0>, dim3(a.M), dim3(64), 0, s, a);
+  if (dtype == 1) hipLaunchKernelGGL(k_norm<1>, dim3(a.M), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_norm<0>, dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -769,20 +744,29 @@ size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
 
 int linear_waves(int n_groups) { return n_groups >= 512 ? 4 : 8; }
 
+// With events, the start / stop timestamps are taken by the dispatch itself
+// (the kernel's own execution, as a kernel trace measures it).
 template <int DT, bool MFMA>
-static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s) {
-  if (linear_waves(a.n_groups) == 4) hipLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), lds, s, a);
-  else hipLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), lds, s, a);
+static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1) {
+  if (linear_waves(a.n_groups) == 4) {
+    if (e0) hipExtLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), (uint32_t)lds, s, e0, e1, 0, a);
+    else hipLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), lds, s, a);
+  } else {
+    if (e0) hipExtLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), (uint32_t)lds, s, e0, e1, 0, a);
+    else hipLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), lds, s, a);
+  }
 }
 
-hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s) {
+hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s, hipEvent_t e0,
+                         hipEvent_t e1) {
   const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
   if (dtype == 1) {
-    if (mfma) launch_linear_t<1, true>(a, grid, lds, s);
-    else launch_linear_t<1, false>(a, grid, lds, s);
+    if (mfma) launch_linear_t<1, true>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<1, false>(a, grid, lds, s, e0, e1);
   } else {
-    if (mfma) launch_linear_t<0, true>(a, grid, lds, s);
-    else launch_linear_t<0, false>(a, grid, lds, s);
+    if (mfma) launch_linear_t<0, true>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<0, false>(a, grid, lds, s, e0, e1);
   }
   return hipGetLastError();
 }

@@ -46,6 +46,7 @@ const char* check_config(const lede_config* c) {
   if (c->head_dim != 64 && c->head_dim != 128) return "head_dim must be 64 or 128";
   if (c->n_heads % c->n_kv_heads) return "n_heads must be a multiple of n_kv_heads";
   if (c->d_model % 32 || (c->n_heads * c->head_dim) % 32) return "d_model and n_heads*head_dim must be multiples of 32";
+  if (c->d_model > 8192) return "d_model above 8192 is not supported";
   if (c->ffn_dim % 8 || c->ffn_dim < 8) return "ffn_dim must be a multiple of 8";
   if (c->vocab % 16) return "vocab must be a multiple of 16";
   if (c->page_size != PAGE) return "page_size must be 64";
@@ -224,6 +225,35 @@ int prof_fold(lede_ctx* c) {
   return LEDE_OK;
 }
 
+// A linear launch: when timing, the dispatch records its own start / end
+// events (kernel execution only).
+int launch_linear_timed(lede_ctx* c, int cls, double bytes, int dt, bool mfma, const LinearArgs& a, int grid,
+                        hipStream_t s) {
+  if (!c->prof) {
+    HIP_CHECK(c, launch_linear(dt, mfma, a, grid, s));
+    return LEDE_OK;
+  }
+  hipEvent_t e0 = next_event(c), e1 = next_event(c);
+  if (!e0 || !e1) return fail(c, LEDE_E_HIP, "hipEventCreate failed");
+  HIP_CHECK(c, launch_linear(dt, mfma, a, grid, s, e0, e1));
+  c->recs.push_back({cls, e0, e1, bytes});
+  return LEDE_OK;
+}
+
+#define LAUNCH_LINEAR(vec, a, dt)                                                                        \
+  do {                                                                                                   \
+    int rc_ = launch_linear_timed(c, linear_class(vec, (a).n_groups), linear_bytes(a, dt), dt, !(vec), a, \
+                                  linear_grid((a).n_groups, (a).epi), s);                               \
+    if (rc_) return rc_;                                                                                 \
+  } while (0)
+
+// Timing class of a linear launch: one per kernel symbol.
+int linear_class(bool vec, int n_groups) {
+  const bool eight = linear_waves(n_groups) == 8;
+  if (vec) return eight ? LEDE_K_LINEAR_VEC8 : LEDE_K_LINEAR_VEC;
+  return eight ? LEDE_K_LINEAR_MFMA8 : LEDE_K_LINEAR_MFMA;
+}
+
 #define LAUNCH(cls, bytes, expr)                         \
   do {                                                   \
     hipEvent_t e0_ = nullptr;                            \
@@ -351,8 +381,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
       qa.x_mode = X_PLAIN; qa.x = c->S<void>(o.xn); qa.ldx = o.d;
     }
-    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(qa, dt),
-           launch_linear(dt, !vec, qa, linear_grid(qa.n_groups, qa.epi), s));
+    LAUNCH_LINEAR(vec, qa, dt);
 
     AttnArgs at{};
     at.q = c->S<float>(o.q); at.ldq = o.qd;
@@ -376,8 +405,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
     oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
     oa.epi = EPI_RESID;
-    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(oa, dt),
-           launch_linear(dt, !vec, oa, linear_grid(oa.n_groups, oa.epi), s));
+    LAUNCH_LINEAR(vec, oa, dt);
 
     // feed-forward block
     LinearArgs ga = base_linear(c);
@@ -395,8 +423,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
       ga.x_mode = X_PLAIN; ga.x = c->S<void>(o.xn); ga.ldx = o.d;
     }
-    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(ga, dt),
-           launch_linear(dt, !vec, ga, linear_grid(ga.n_groups, ga.epi), s));
+    LAUNCH_LINEAR(vec, ga, dt);
 
     LinearArgs da = base_linear(c);
     da.M = M;
@@ -404,8 +431,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
     da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
     da.epi = EPI_RESID;
-    LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(da, dt),
-           launch_linear(dt, !vec, da, linear_grid(da.n_groups, da.epi), s));
+    LAUNCH_LINEAR(vec, da, dt);
 
     if (qnet_after == j + 1 && o.H > 0) {
       NormArgs na{};
@@ -448,8 +474,7 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
     LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(o.dt, na, s));
     ha.x_mode = X_PLAIN; ha.x = c->S<void>(o.xn); ha.ldx = o.d;
   }
-  LAUNCH(vec ? LEDE_K_LINEAR_VEC : LEDE_K_LINEAR_MFMA, linear_bytes(ha, o.dt),
-         launch_linear(o.dt, !vec, ha, linear_grid(ha.n_groups, ha.epi), s));
+  LAUNCH_LINEAR(vec, ha, o.dt);
   return LEDE_OK;
 }
 

@@ -42,9 +42,12 @@ class LedeProfEntry(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double), ("bytes", ctypes.c_double), ("launches", ctypes.c_int64)]
 
 
-K_LINEAR_VEC, K_LINEAR_MFMA, K_ATTENTION, K_NORM, K_QNET, K_ACCEPT, K_DRAFT_PHASE, K_VERIFY_PHASE = range(8)
-K_NCLASS = 8
-K_NAMES = ["linear_vec", "linear_mfma", "attention", "norm", "qnet", "accept", "draft_phase", "verify_phase"]
+K_NCLASS = 10
+K_NAMES = ["linear_vec", "linear_mfma", "attention", "norm", "qnet", "accept", "draft_phase", "verify_phase",
+           "linear_vec8", "linear_mfma8"]
+# rocprofv3 kernel symbol of each linear timing class (bf16 models)
+K_SYMBOLS = {"linear_vec": "lede::k_linear<1, false, 4>", "linear_mfma": "lede::k_linear<1, true, 4>",
+             "linear_vec8": "lede::k_linear<1, false, 8>", "linear_mfma8": "lede::k_linear<1, true, 8>"}
 
 
 class LedeAction(ctypes.Structure):
