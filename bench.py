@@ -10,9 +10,12 @@ truncation.  Inputs are synthetic and already resident in HBM when timing
 starts.
 
 Prints one JSON line: tokens/s over the timed steps, the HBM roofline of the
-dominant kernel (algorithmic bytes / HIP-event duration, from a second,
-instrumented replay of the same steps) and the CPU oracle timed on a bounded
-sample of the same workload.
+dominant kernel (algorithmic bytes / HIP-event duration, from an instrumented
+replay of the same steps), per-pass rates (draft and verify phases timed in a
+replay with no other events), plain autoregressive decoding on the same path
+(verify with no drafts), the achievable read bandwidth of the weight arena
+(a read-once probe kernel), and the CPU oracle timed on a bounded sample of
+the same workload.
 """
 from __future__ import annotations
 
@@ -183,17 +186,46 @@ def main():
     log("timed %d steps: %.3f ms/step (wall %.3f ms/step), %d tokens" % (args.steps, ms / args.steps,
                                                                         1e3 * wall / args.steps, toks))
 
-    # instrumented replay of the same steps from the prompt state
+    def replay(level, n):
+        """The same steps again from the prompt state, timed at a level."""
+        eng.lede_truncate(wl.prompt_len)
+        eng.lede_set_pending(first)
+        del produced[1:]
+        for _ in range(min(args.warmup, 3)):
+            step()
+        eng.lede_prof_enable(level)
+        eng.lede_prof_read(reset=True)
+        rs = [step() for _ in range(n)]
+        pr = eng.lede_prof_read(reset=True)
+        eng.lede_prof_enable(0)
+        return rs, pr
+
+    # draft / verify phase times with nothing else recorded, then every launch
+    phase_recs, phases = replay(1, args.prof_steps)
+    prof_recs, prof = replay(2, args.prof_steps)
+
+    # plain autoregressive decoding on the same path (verify with no drafts)
     eng.lede_truncate(wl.prompt_len)
     eng.lede_set_pending(first)
     del produced[1:]
+    n_ar = min(args.steps, wl.n_gen - 2)
     for _ in range(min(args.warmup, 3)):
-        step()
-    eng.lede_prof_enable(True)
-    eng.lede_prof_read(reset=True)
-    prof_recs = [step() for _ in range(args.prof_steps)]
-    prof = eng.lede_prof_read(reset=True)
-    eng.lede_prof_enable(False)
+        eng.lede_step((l, 0), log_qnet=False)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    ar_recs = [eng.lede_step((l, 0), log_qnet=False) for _ in range(n_ar)]
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ar_ms = e0.elapsed_time(e1)
+    ar_bytes = sum(verify_bytes(m, 0, r.seq_len - 1) for r in ar_recs)
+
+    # achievable read bandwidth: the weight arena read once by the probe kernel
+    from paper_2606_03113_amd import op_read_probe
+    probe_bytes = eng.weights.numel() // 16 * 16
+    probe = {}
+    for grid in (1024, 4096, 16384):
+        op_read_probe(eng.weights[:probe_bytes], grid)
+        probe[grid] = probe_bytes / (min(op_read_probe(eng.weights[:probe_bytes], grid) for _ in range(3)) * 1e6)
     from paper_2606_03113_amd.lede import K_SYMBOLS
     lin = {n: prof[n] for n in K_SYMBOLS}
     dom = max(lin, key=lambda n: lin[n]["ms"])
@@ -201,10 +233,10 @@ def main():
     achieved = d["bytes"] / (d["ms"] * 1e6)  # GB/s
     kname = K_SYMBOLS[dom]
     traffic = traffic_from_profile(dom, wl.name, d["launches"])
-    dp, vp = prof["draft_phase"], prof["verify_phase"]
-    # algorithmic bytes of the instrumented steps' passes
+    dp, vp = phases["draft_phase"], phases["verify_phase"]
+    # algorithmic bytes of the phase-timed steps' passes
     db = vb = 0.0
-    for r in prof_recs:
+    for r in phase_recs:
         c = r.seq_len - r.accepted - 1  # KV length when the step started
         db += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff)) + (m.qnet_bytes() if log_q else 0)
         vb += verify_bytes(m, r.k_eff, c)
@@ -240,10 +272,17 @@ def main():
             "verify_GBps": round(vb / (vp["ms"] * 1e6), 1) if vp["ms"] else None,
             "draft_frac": round(db / (dp["ms"] * 1e6) / HBM_PEAK_GBPS, 4) if dp["ms"] else None,
             "verify_frac": round(vb / (vp["ms"] * 1e6) / HBM_PEAK_GBPS, 4) if vp["ms"] else None,
-            "kernel_ms": {n: round(v["ms"] / args.prof_steps, 4) for n, v in prof.items()},
+            "kernel_ms": {n: round(v["ms"] / args.prof_steps, 4) for n, v in prof.items()
+                          if not n.endswith("_phase")},
         },
         "acceptance": {"accepted": accepted, "drafted": drafted,
                        "acc_rate": round(accepted / drafted, 4) if drafted else None},
+        "ar": {"tokens_per_s": round(n_ar / (ar_ms / 1e3), 3), "ms_per_token": round(ar_ms / n_ar, 4),
+               "GBps": round(ar_bytes / (ar_ms * 1e6), 1), "frac": round(ar_bytes / (ar_ms * 1e6) / HBM_PEAK_GBPS, 4),
+               "ssd_speedup": round((acc_tokens / (ms / 1e3)) / (n_ar / (ar_ms / 1e3)), 4)},
+        "hbm_read_probe": {"GBps": round(max(probe.values()), 1),
+                           "frac": round(max(probe.values()) / HBM_PEAK_GBPS, 4),
+                           "bytes": probe_bytes, "by_grid": {str(g): round(v, 1) for g, v in probe.items()}},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

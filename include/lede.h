@@ -194,9 +194,10 @@ int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats
                     void* stream);
 
 /* ---- timing for roofline reports ------------------------------------------
- * When enabled, every kernel launch is bracketed by a pair of HIP events on
- * its stream and attributed to a kernel class; the draft phase and the
- * verify phase of each lede_step are bracketed as well.  Reading
+ * Level 1 brackets the draft phase and the verify phase of each lede_step
+ * with HIP events on its stream.  Level 2 also has every kernel launch record
+ * its own start / end events and attributes it to a kernel class (the extra
+ * events slow the phases down, so phase rates are read at level 1).  Reading
  * synchronises, converts the event pairs to milliseconds and (reset != 0)
  * clears the totals.  bytes is the algorithmic HBM traffic of the launches:
  * weights and KV read once, plus activations in and out. */
@@ -219,7 +220,7 @@ typedef struct {
   int64_t launches;
 } lede_prof_entry;
 
-int lede_prof_enable(lede_ctx* ctx, int32_t on);
+int lede_prof_enable(lede_ctx* ctx, int32_t level /* 0 off, 1 phases, 2 phases + launches; else LEDE_E_ARG */);
 int lede_prof_read(lede_ctx* ctx, lede_prof_entry* out /* [LEDE_K_NCLASS] */, int32_t reset);
 
 /* ---- single-operation entry points (kernel-level tests and tooling) ----- */
@@ -237,6 +238,16 @@ int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* t
  * matrix-core kernel of the verify path. */
 int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M,
                    float* y, int32_t use_mfma, void* stream);
+
+/* Achievable HBM read bandwidth: reads `bytes` (a multiple of 16, > 0) of the
+ * device buffer src once, with the same non-temporal 16-byte loads the
+ * linear kernels use for weights, on `grid` (1..65535) blocks of 256 threads;
+ * one uint32 per block goes to the device buffer sink [grid] so that no load
+ * is dropped.  kernel_ms (nullable host pointer): when given, the dispatch
+ * records its own start / end events, the call waits for them and stores the
+ * kernel's duration.  LEDE_E_ARG on bad arguments, LEDE_E_HIP on a HIP error. */
+int lede_op_read_probe(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream,
+                       float* kernel_ms);
 
 #ifdef __cplusplus
 }

@@ -150,6 +150,10 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
+// Reads bytes (a multiple of 16) of src once; e0 / e1 (may be null) bracket
+// the kernel's execution.
+hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t s,
+                             hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
 
 // Wavefronts per block of the linear kernel for a matrix of n_groups row groups.

@@ -720,6 +720,32 @@ __global__ void k_set_token(uint64_t* keys, int idx, int token) {
   if (threadIdx.x == 0) keys[idx] = (uint64_t)(0xFFFFFFFFu - (uint32_t)token);
 }
 
+// Achievable-bandwidth probe: every 16-byte chunk of src is read once with
+// the same non-temporal loads the linear kernels stream weights with, eight
+// loads in flight per lane; the XOR of the data goes to sink[block] so that no
+// load can be dropped.
+__global__ __launch_bounds__(256) void k_read_probe(const uint8_t* src, size_t n16, uint32_t* sink) {
+  const size_t stride = (size_t)gridDim.x * 256;
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    uint4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ld16_stream(src + (i + u * stride) * 16);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n16; i += stride) {
+    const uint4 v = ld16_stream(src + i * 16);
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  __shared__ uint32_t red[4];
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
 // ---- launchers ----------------------------------------------------------------
 
 hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
@@ -803,6 +829,16 @@ hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s) {
 
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t s,
+                             hipEvent_t e0, hipEvent_t e1) {
+  if (e0)
+    hipExtLaunchKernelGGL(k_read_probe, dim3(grid), dim3(256), 0, s, e0, e1, 0, (const uint8_t*)src, bytes / 16,
+                          sink);
+  else
+    hipLaunchKernelGGL(k_read_probe, dim3(grid), dim3(256), 0, s, (const uint8_t*)src, bytes / 16, sink);
   return hipGetLastError();
 }
 

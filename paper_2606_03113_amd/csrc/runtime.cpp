@@ -144,9 +144,10 @@ struct lede_ctx {
   int last_rows = 0, last_draft_rows = 0;
   std::string err;
 
-  // timing (lede_prof_*): event pairs per launch, folded into per-class totals
+  // timing (lede_prof_*): event pairs folded into per-class totals;
+  // level 1 brackets the draft and verify phases, level 2 also every launch
   struct ProfRec { int cls; hipEvent_t a, b; double bytes; };
-  bool prof = false;
+  int prof = 0;
   std::vector<hipEvent_t> evpool;
   size_t ev_next = 0;
   std::vector<ProfRec> recs;
@@ -191,9 +192,9 @@ hipEvent_t next_event(lede_ctx* c) {
   return c->evpool[c->ev_next++];
 }
 
-int prof_mark(lede_ctx* c, hipStream_t s, hipEvent_t* e) {
+int prof_mark(lede_ctx* c, hipStream_t s, hipEvent_t* e, int level = 2) {
   *e = nullptr;
-  if (!c->prof) return LEDE_OK;
+  if (c->prof < level) return LEDE_OK;
   *e = next_event(c);
   if (!*e) return fail(c, LEDE_E_HIP, "hipEventCreate failed");
   HIP_CHECK(c, hipEventRecord(*e, s));
@@ -203,7 +204,7 @@ int prof_mark(lede_ctx* c, hipStream_t s, hipEvent_t* e) {
 int prof_close(lede_ctx* c, hipStream_t s, int cls, double bytes, hipEvent_t e0) {
   if (!c->prof || !e0) return LEDE_OK;
   hipEvent_t e1 = nullptr;
-  int rc = prof_mark(c, s, &e1);
+  int rc = prof_mark(c, s, &e1, 1);
   if (rc) return rc;
   c->recs.push_back({cls, e0, e1, bytes});
   return LEDE_OK;
@@ -229,7 +230,7 @@ int prof_fold(lede_ctx* c) {
 // events (kernel execution only).
 int launch_linear_timed(lede_ctx* c, int cls, double bytes, int dt, bool mfma, const LinearArgs& a, int grid,
                         hipStream_t s) {
-  if (!c->prof) {
+  if (c->prof < 2) {
     HIP_CHECK(c, launch_linear(dt, mfma, a, grid, s));
     return LEDE_OK;
   }
@@ -804,7 +805,7 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   const int l_min = o.H ? c->cfg.exits[0] : 0;
   const bool want_q = o.H && (!forced || log_qnet);
   hipEvent_t ph0 = nullptr;
-  if ((rc0 = prof_mark(c, s, &ph0))) return rc0;
+  if ((rc0 = prof_mark(c, s, &ph0, 1))) return rc0;
   int k_eff = forced ? std::min(k, n_remaining - 1) : std::min(o.k_max, n_remaining - 1);
   bool ran_q = false;
   int rc;
@@ -841,7 +842,7 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   }
   if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
   hipEvent_t ph1 = nullptr;
-  if ((rc = prof_mark(c, s, &ph1))) return rc;
+  if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
   rc = launch_verify(c, k_eff, s);
   if (rc) return rc;
   if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
@@ -913,7 +914,8 @@ int lede_prof_enable(lede_ctx* c, int32_t on) {
   if (!c) return LEDE_E_ARG;
   int rc = prof_fold(c);
   if (rc) return rc;
-  c->prof = on != 0;
+  if (on < 0 || on > 2) return fail(c, LEDE_E_ARG, "timing level %d not in 0..2", on);
+  c->prof = on;
   return LEDE_OK;
 }
 
@@ -956,6 +958,23 @@ int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const
   a.epi = EPI_STORE; a.out = y; a.ldo = N;
   return launch_linear(dtype, use_mfma != 0, a, std::min(a.n_groups, 4096), S_(stream)) == hipSuccess ? LEDE_OK
                                                                                                   : LEDE_E_HIP;
+}
+
+int lede_op_read_probe(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream, float* kernel_ms) {
+  if (!src || !sink || bytes == 0) return LEDE_E_ARG;
+  if (bytes % 16 || grid < 1 || grid > 65535) return LEDE_E_ARG;
+  if (!kernel_ms)
+    return launch_read_probe(src, bytes, sink, grid, S_(stream)) == hipSuccess ? LEDE_OK : LEDE_E_HIP;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess) return LEDE_E_HIP;
+  if (hipEventCreate(&e1) != hipSuccess) { (void)hipEventDestroy(e0); return LEDE_E_HIP; }
+  int rc = LEDE_OK;
+  if (launch_read_probe(src, bytes, sink, grid, S_(stream), e0, e1) != hipSuccess ||
+      hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(kernel_ms, e0, e1) != hipSuccess)
+    rc = LEDE_E_HIP;
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return rc;
 }
 
 }  // extern "C"

@@ -64,7 +64,8 @@ class LedeStepRecord(ctypes.Structure):
 EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error", "lede_load_tensor",
             "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
-            "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear"]
+            "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
+            "lede_op_read_probe"]
 
 _lib = None
 
@@ -102,6 +103,7 @@ def load(path: str = LIB_PATH):
     L.lede_op_tiled_bytes.restype = sz
     L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
     L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, vp, i32, vp]
+    L.lede_op_read_probe.argtypes = [vp, sz, vp, i32, vp, P(ctypes.c_float)]
     for name in EXPORTED:
         if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes"):
             getattr(L, name).restype = ctypes.c_int
@@ -280,8 +282,9 @@ class Engine:
                                            n_floats, ctypes.byref(rows), self.stream), self.ctx)
         return out, rows.value
 
-    def lede_prof_enable(self, on: bool):
-        self._check(self.L.lede_prof_enable(self.ctx, int(on)), self.ctx)
+    def lede_prof_enable(self, level: int):
+        """0 off, 1 draft / verify phases only, 2 phases and every launch."""
+        self._check(self.L.lede_prof_enable(self.ctx, int(level)), self.ctx)
 
     def lede_prof_read(self, reset: bool = True) -> dict:
         arr = (LedeProfEntry * K_NCLASS)()
@@ -318,3 +321,19 @@ def op_linear(W, x, use_mfma: bool):
     if rc:
         raise LedeError(rc, "op_linear")
     return y
+
+
+def op_read_probe(buf, grid: int = 0) -> float:
+    """Kernel milliseconds for one read of the whole GPU tensor buf (its byte
+    size a multiple of 16) with the weight-streaming loads."""
+    import torch
+    L = load()
+    nbytes = buf.numel() * buf.element_size()
+    grid = grid or 256 * 16
+    sink = torch.empty(grid, dtype=torch.int32, device=buf.device)
+    ms = ctypes.c_float()
+    s = ctypes.c_void_p(torch.cuda.current_stream(buf.device).cuda_stream)
+    rc = L.lede_op_read_probe(buf.data_ptr(), nbytes, sink.data_ptr(), int(grid), s, ctypes.byref(ms))
+    if rc:
+        raise LedeError(rc, "op_read_probe")
+    return ms.value

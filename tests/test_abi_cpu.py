@@ -78,3 +78,15 @@ def test_null_arguments(lib):
     out = ctypes.c_void_p()
     assert lib.lede_create(None, None, 0, None, 0, None, 0, ctypes.byref(out)) == lede.LEDE_E_ARG
     assert lib.lede_last_error(None) == b"null context"
+
+
+def test_read_probe_rejects_bad_arguments(lib):
+    from paper_2606_03113_amd import lede
+    sink = ctypes.c_void_p(16)
+    src = ctypes.c_void_p(4096)
+    assert lib.lede_op_read_probe(None, 1024, sink, 4, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_probe(src, 1000, sink, 4, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_probe(src, 0, sink, 4, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_probe(src, 1024, sink, 0, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_probe(src, 1024, sink, 65536, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_probe(src, 1024, None, 4, None, None) == lede.LEDE_E_ARG

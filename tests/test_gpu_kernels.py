@@ -82,3 +82,19 @@ def test_mfma_rows_independent_of_batch():
     for m in (0, 4, 8):
         y1 = op_linear(Wd, xd[m:m + 1].contiguous(), True)
         assert torch.equal(y1[0], y9[m])
+
+
+@pytest.mark.parametrize("n_words,grid", [(4, 1), (1000, 3), (1 << 20, 4096), ((1 << 20) + 12, 257)])
+def test_read_probe_reads_every_word(n_words, grid):
+    """The bandwidth probe touches every 16-byte chunk exactly once: the XOR
+    of its per-block results equals the XOR of all words."""
+    from paper_2606_03113_amd import op_read_probe, load
+    import ctypes
+    words = li.uniform_int(5, 9, n_words, 0, (1 << 31) - 1).view(np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).to("cuda")
+    sink = torch.zeros(grid, dtype=torch.int32, device="cuda")
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert load().lede_op_read_probe(buf.data_ptr(), n_words * 4, sink.data_ptr(), grid, s, None) == 0
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(words)
+    assert op_read_probe(buf) > 0
