@@ -126,6 +126,9 @@ def main():
     from lede_inputs.configs import WORKLOADS
     from paper_2606_03113_amd import Engine
 
+    if args.graphs:
+        # captured graphs need a stream other than the legacy default one
+        torch.cuda.set_stream(torch.cuda.Stream())
     wl = WORKLOADS[args.workload]
     m = wl.model
     l, k = wl.fixed

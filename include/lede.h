@@ -202,16 +202,15 @@ int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats
  * clears the totals.  bytes is the algorithmic HBM traffic of the launches:
  * weights and KV read once, plus activations in and out. */
 enum {
-  LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel, 4 wavefronts (draft path, >= 512 row groups) */
-  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel, 4 wavefronts (verify / prefill path) */
+  LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel, input row staged in LDS (draft path) */
+  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel (verify / prefill path) */
   LEDE_K_ATTENTION,       /* paged attention partial + combine */
   LEDE_K_NORM,            /* RMSNorm rows */
   LEDE_K_QNET,            /* Q-network layers */
   LEDE_K_ACCEPT,          /* acceptance scan + KV truncation */
   LEDE_K_DRAFT_PHASE,     /* all draft passes of a step */
   LEDE_K_VERIFY_PHASE,    /* the verify pass + acceptance of a step */
-  LEDE_K_LINEAR_VEC8,     /* one-row linear kernel, 8 wavefronts (< 512 row groups) */
-  LEDE_K_LINEAR_MFMA8,    /* matrix-core linear kernel, 8 wavefronts */
+  LEDE_K_LINEAR_VEC_GX,   /* one-row linear kernel, input row read from global memory (rows > 32 KiB) */
   LEDE_K_NCLASS
 };
 typedef struct {

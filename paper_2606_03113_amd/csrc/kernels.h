@@ -156,8 +156,20 @@ hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int 
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
 
-// Wavefronts per block of the linear kernel for a matrix of n_groups row groups.
-int linear_waves(int n_groups);
+// Linear kernel shape: wavefronts per block, and where the input row comes
+// from (see k_linear).  Rows longer than LIN_LDS_X_MAX bytes are read from
+// global memory instead of being staged in LDS.
+constexpr int LIN_WAVES = 8;
+constexpr int LIN_LDS_X_MAX = 32768;
+constexpr int LIN_TILES_PER_WAVE = 4;  // tiles each wavefront has in flight per batch
+enum XSource { XS_LDS = 0, XS_GLOBAL = 1, XS_MFMA = 2 };
+// K tiles the staged row is zero-padded to, so that every batch reads it
+// without bounds checks.
+__host__ __device__ inline int lin_x_tiles(int KT) {
+  const int b = LIN_WAVES * LIN_TILES_PER_WAVE;
+  return (KT + b - 1) / b * b;
+}
+int linear_x_source(int dtype, bool mfma, int K);
 
 // Bytes of dynamic LDS the linear kernels use for the staged input row.
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M);

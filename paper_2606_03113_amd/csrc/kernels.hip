@@ -339,11 +339,16 @@ __device__ __forceinline__ float block_sum(float v, float* scratch) {
 }
 
 // Normalise the single input row of the vector kernel into LDS with every
-// thread of the block (thread t holds elements 4t + 4 NT j in registers).
+// thread of the block: the raw row goes to an fp32 LDS copy (thread t loads
+// elements 4t + 4 NT j) while the sum of squares accumulates in j order, then
+// the normalised row is written in the model dtype for the dot products.
 template <int DT, int NW>
 __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch) {
   constexpr int NT = NW * 64;
   const int tid = threadIdx.x;
+  const int row_bytes = a.K * Elem<DT>::ES_, pad_bytes = lin_x_tiles(a.KT) * Tile<DT>::TK * Elem<DT>::ES_;
+  float* raw = (float*)(lds + pad_bytes);
+  for (int i = row_bytes + tid * 4; i < pad_bytes; i += NT * 4) *(uint32_t*)(lds + i) = 0u;
   const float* h = a.h;
   const void* row = nullptr;
   float* h_out = nullptr;
@@ -353,63 +358,70 @@ __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch
     if (blockIdx.x == 0) h_out = a.h;
     h = nullptr;
   }
-  float4 v[8];
   float ss = 0.f;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = 4 * tid + 4 * NT * j;
-    v[j] = i < a.K ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    ss = fmaf(v[j].x, v[j].x, ss);
-    ss = fmaf(v[j].y, v[j].y, ss);
-    ss = fmaf(v[j].z, v[j].z, ss);
-    ss = fmaf(v[j].w, v[j].w, ss);
+#pragma unroll 4
+  for (int i = 4 * tid; i < a.K; i += 4 * NT) {
+    const float4 v = row_load4<DT>(h, row, i);
+    *(float4*)(raw + i) = v;
+    if (h_out) *(float4*)(h_out + i) = v;
+    ss = fmaf(v.x, v.x, ss);
+    ss = fmaf(v.y, v.y, ss);
+    ss = fmaf(v.z, v.z, ss);
+    ss = fmaf(v.w, v.w, ss);
   }
   ss = block_sum<NW>(ss, scratch);
   const float inv = rsqrtf(ss / (float)a.K + a.eps);
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = 4 * tid + 4 * NT * j;
-    if (i < a.K) {
-      const float4 g = row_load4<DT>(nullptr, a.gain, i);
-      float4 y;
-      y.x = (v[j].x * inv) * g.x;
-      y.y = (v[j].y * inv) * g.y;
-      y.z = (v[j].z * inv) * g.z;
-      y.w = (v[j].w * inv) * g.w;
-      if (h_out) *(float4*)(h_out + i) = v[j];
-      store4<DT>(lds, i, y);
-    }
+#pragma unroll 4
+  for (int i = 4 * tid; i < a.K; i += 4 * NT) {
+    const float4 v = *(const float4*)(raw + i);
+    const float4 g = row_load4<DT>(nullptr, a.gain, i);
+    float4 y;
+    y.x = (v.x * inv) * g.x;
+    y.y = (v.y * inv) * g.y;
+    y.z = (v.z * inv) * g.z;
+    y.w = (v.w * inv) * g.w;
+    store4<DT>(lds, i, y);
   }
   __syncthreads();
 }
 
-// y = W x over 16-row groups, one group per block.  NW waves split K (wave w
-// takes tiles w, w + NW, ...) and the partials are summed in wave order.
-// Vector kernel: one input row, dot2 instructions, the input row normalised
-// in the prologue (X_NORM / X_EMBED_NORM) or read from global memory.
-// Matrix kernel: up to 16 rows read from global memory (normalised by the
-// norm kernel), 16x16 matrix-core tiles.
-template <int DT, bool MFMA, int NW>
-__global__ __launch_bounds__(NW * 64) void k_linear(LinearArgs a) {
+// Copy the vector kernel's input row (KT tiles of the model dtype) into LDS
+// and zero the padding up to pad bytes.
+template <int NW>
+__device__ void stage_copy_row(const void* x, int bytes, int pad, uint8_t* lds) {
+  for (int i = threadIdx.x * 16; i < pad; i += NW * 64 * 16)
+    *(uint4*)(lds + i) = i < bytes ? ld16((const uint8_t*)x + i) : make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+}
+
+// y = W x over 16-row groups, one group per block pass.  Eight wavefronts
+// split K (wave w takes tiles w, w + 8, ...), four tiles per wave in flight,
+// and the partials are summed in wave order.
+//   XS = XS_LDS:    one input row, staged in LDS in the prologue (normalised
+//                   for X_NORM / X_EMBED_NORM, copied otherwise); dot2 math.
+//   XS = XS_GLOBAL: one input row read from global memory per tile (rows too
+//                   long for LDS); dot2 math.
+//   XS = XS_MFMA:   up to 16 rows read from global memory (normalised by the
+//                   norm kernel), 16x16 matrix-core tiles.
+template <int DT, int XS>
+__global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   typedef Tile<DT> TL;
-  constexpr int U = NW >= 8 ? 4 : 8;  // tiles per wave per batch
+  constexpr int NW = LIN_WAVES, U = 4;  // tiles per wave per batch
+  constexpr bool MFMA = XS == XS_MFMA;
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ float red[NW][16][16];
   __shared__ float ct[16][17];
   __shared__ float scratch[NW];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int KT = a.KT, NG = a.n_groups;
-  const bool staged = !MFMA && (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM);
   const uint4 zero = {0u, 0u, 0u, 0u};
 
   if (blockIdx.x == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
 
   int g = blockIdx.x;
   // the weights do not depend on the input: the first batch is in flight
-  // while the prologue normalises the input row
+  // while the prologue stages the input row
   uint4 w[U];
   {
     const uint8_t* wg = a.w + (size_t)(g < NG ? g : 0) * KT * TILE_BYTES + lane * 16;
@@ -419,20 +431,22 @@ __global__ __launch_bounds__(NW * 64) void k_linear(LinearArgs a) {
       w[u] = (g < NG && t < KT) ? ld16_stream(wg + (size_t)t * TILE_BYTES) : zero;
     }
   }
-  if (staged) stage_norm_row<DT, NW>(a, smem, scratch);
+  if (XS == XS_LDS) {
+    if (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM) stage_norm_row<DT, NW>(a, smem, scratch);
+    else stage_copy_row<NW>(a.x, KT * TL::TK * TL::ES, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
+  }
 
   uint64_t best = 0;
   bool first = true;
   for (; g < NG; g += gridDim.x, first = false) {
     const uint8_t* wg = a.w + (size_t)g * KT * TILE_BYTES + lane * 16;
-    const int m = MFMA ? (lane & 15) : 0;
-    const bool has = m < (MFMA ? a.M : 1);
-    const uint8_t* xb = staged ? smem + (size_t)(lane >> 4) * 16
-                               : (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
     float acc0 = 0.f, acc1 = 0.f;
     f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+    const int m = MFMA ? (lane & 15) : 0;
+    const bool has = !MFMA || m < a.M;
+    const uint8_t* xg = (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
+    const uint8_t* xs = smem + (lane >> 4) * 16;
     for (int t = wave; t < KT; t += NW * U) {
-      uint4 x[U];
       if (!(first && t == wave)) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -440,22 +454,31 @@ __global__ __launch_bounds__(NW * 64) void k_linear(LinearArgs a) {
           w[u] = tt < KT ? ld16_stream(wg + (size_t)tt * TILE_BYTES) : zero;
         }
       }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int tt = t + NW * u;
-        x[u] = (has && tt < KT) ? ld16(xb + (size_t)tt * TL::TK * TL::ES) : zero;
-      }
-      if (MFMA) {
+      if (XS == XS_LDS) {
 #pragma unroll
         for (int u = 0; u < U; u += 2) {
-          c0 = mfma_tile<DT>(w[u], x[u], c0);
-          c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
+          const int t0 = t + NW * u, t1 = t0 + NW;  // the staged row is zero-padded past KT
+          const uint4 x0 = *(const uint4*)(xs + (size_t)t0 * TL::TK * TL::ES);
+          const uint4 x1 = *(const uint4*)(xs + (size_t)t1 * TL::TK * TL::ES);
+          acc0 = dot16<DT>(w[u], x0, acc0);
+          acc1 = dot16<DT>(w[u + 1], x1, acc1);
         }
       } else {
+        uint4 x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int tt = t + NW * u;
+          x[u] = (has && tt < KT) ? ld16(xg + (size_t)tt * TL::TK * TL::ES) : zero;
+        }
 #pragma unroll
         for (int u = 0; u < U; u += 2) {
-          acc0 = dot16<DT>(w[u], x[u], acc0);
-          acc1 = dot16<DT>(w[u + 1], x[u + 1], acc1);
+          if (MFMA) {
+            c0 = mfma_tile<DT>(w[u], x[u], c0);
+            c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
+          } else {
+            acc0 = dot16<DT>(w[u], x[u], acc0);
+            acc1 = dot16<DT>(w[u + 1], x[u + 1], acc1);
+          }
         }
       }
     }
@@ -527,7 +550,32 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   const int n_chunks = pmax / 64 + 1;
   if ((int)blockIdx.y >= n_chunks) return;
   const float scale = rsqrtf((float)HD);
-  int page = a.block_table[blockIdx.y];  // in flight with the query loads
+  // thread roles: scores (token t, part p covering dims p*8 + 32c + e);
+  // values (dims dg*8.., tokens tg + PV_TG u)
+  const int dg = tid % PV_DG, tg = tid / PV_DG;
+  float vf[TPT][8], kf[NPC * 8];
+  auto load_page = [&](int jj) {
+    const int page = a.block_table[jj];
+    const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
+    const int nvalid = min(64, pmax - jj * 64 + 1);
+#pragma unroll
+    for (int u = 0; u < TPT; ++u) {
+      const int t = tg + PV_TG * u;
+      if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
+      else
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
+    }
+    const int t = tid >> 2, p = tid & 3;
+    if (t < nvalid) {
+#pragma unroll
+      for (int c = 0; c < NPC; ++c) load8<DT>(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c, kf + 8 * c);
+    } else {
+#pragma unroll
+      for (int e = 0; e < NPC * 8; ++e) kf[e] = 0.f;
+    }
+  };
+  load_page(blockIdx.y);  // the first page's keys and values are in flight with the query loads
 
   for (int idx = tid; idx < nr * (HD / 4); idx += 256) {
     const int r = idx / (HD / 4), i = 4 * (idx % (HD / 4));
@@ -541,30 +589,9 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   __syncthreads();
 
   for (int j = blockIdx.y; j < n_chunks; j += a.n_split) {
-    const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
     const int tok0 = j * 64;
-    const int nvalid = min(64, pmax - tok0 + 1);
-    if (j + a.n_split < n_chunks) page = a.block_table[j + a.n_split];
-    const int dg = tid % PV_DG, tg = tid / PV_DG;
-    float vf[TPT][8];  // values are loaded together with the keys
-#pragma unroll
-    for (int u = 0; u < TPT; ++u) {
-      const int t = tg + PV_TG * u;
-      if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
-    }
-    {  // scores: thread (token t, part p) covers dims p*8 + 32c + e
+    {
       const int t = tid >> 2, p = tid & 3;
-      float kf[NPC * 8];
-      if (t < nvalid) {
-#pragma unroll
-        for (int c = 0; c < NPC; ++c) load8<DT>(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c, kf + 8 * c);
-      } else {
-#pragma unroll
-        for (int e = 0; e < NPC * 8; ++e) kf[e] = 0.f;
-      }
       for (int r = 0; r < nr; ++r) {
         float s = 0.f;
 #pragma unroll
@@ -611,6 +638,7 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
       }
     }
     __syncthreads();
+    if (j + a.n_split < n_chunks) load_page(j + a.n_split);  // the next page of this block
     for (int idx = tid; idx < nr * HD; idx += 256) {
       const int r = idx / HD, i = idx % HD;
       const int rr = r0 + r, m = rr / G, head = kvh * G + rr % G;
@@ -762,37 +790,44 @@ hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
-  (void)M;
-  if (mfma || (x_mode != X_NORM && x_mode != X_EMBED_NORM)) return 0;
-  return (size_t)K * (dtype == 1 ? 2 : 4);
+int linear_x_source(int dtype, bool mfma, int K) {
+  if (mfma) return XS_MFMA;
+  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
+  return (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es <= LIN_LDS_X_MAX ? XS_LDS : XS_GLOBAL;
 }
 
-int linear_waves(int n_groups) { return n_groups >= 512 ? 4 : 8; }
+size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
+  (void)M;
+  if (linear_x_source(dtype, mfma, K) != XS_LDS) return 0;
+  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
+  const size_t row = (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es;
+  // the norm prologue keeps an fp32 copy of the raw row next to the result
+  return (x_mode == X_NORM || x_mode == X_EMBED_NORM) ? row + (size_t)K * 4 : row;
+}
 
 // With events, the start / stop timestamps are taken by the dispatch itself
 // (the kernel's own execution, as a kernel trace measures it).
-template <int DT, bool MFMA>
+template <int DT, int XS>
 static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                             hipEvent_t e1) {
-  if (linear_waves(a.n_groups) == 4) {
-    if (e0) hipExtLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), (uint32_t)lds, s, e0, e1, 0, a);
-    else hipLaunchKernelGGL((k_linear<DT, MFMA, 4>), dim3(grid), dim3(256), lds, s, a);
-  } else {
-    if (e0) hipExtLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), (uint32_t)lds, s, e0, e1, 0, a);
-    else hipLaunchKernelGGL((k_linear<DT, MFMA, 8>), dim3(grid), dim3(512), lds, s, a);
-  }
+  if (e0)
+    hipExtLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), (uint32_t)lds, s, e0, e1, 0, a);
+  else
+    hipLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), lds, s, a);
 }
 
 hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s, hipEvent_t e0,
                          hipEvent_t e1) {
   const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
+  const int xs = linear_x_source(dtype, mfma, a.K);
   if (dtype == 1) {
-    if (mfma) launch_linear_t<1, true>(a, grid, lds, s, e0, e1);
-    else launch_linear_t<1, false>(a, grid, lds, s, e0, e1);
+    if (xs == XS_MFMA) launch_linear_t<1, XS_MFMA>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_LDS) launch_linear_t<1, XS_LDS>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<1, XS_GLOBAL>(a, grid, lds, s, e0, e1);
   } else {
-    if (mfma) launch_linear_t<0, true>(a, grid, lds, s, e0, e1);
-    else launch_linear_t<0, false>(a, grid, lds, s, e0, e1);
+    if (xs == XS_MFMA) launch_linear_t<0, XS_MFMA>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_LDS) launch_linear_t<0, XS_LDS>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<0, XS_GLOBAL>(a, grid, lds, s, e0, e1);
   }
   return hipGetLastError();
 }

@@ -10,6 +10,7 @@
 #include <deque>
 #include <map>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "../../include/lede.h"
@@ -141,6 +142,8 @@ struct lede_ctx {
   int32_t* record_h = nullptr;  // pinned read-back of the step record
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
+  // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
   std::string err;
 
@@ -243,16 +246,18 @@ int launch_linear_timed(lede_ctx* c, int cls, double bytes, int dt, bool mfma, c
 
 #define LAUNCH_LINEAR(vec, a, dt)                                                                        \
   do {                                                                                                   \
-    int rc_ = launch_linear_timed(c, linear_class(vec, (a).n_groups), linear_bytes(a, dt), dt, !(vec), a, \
+    int rc_ = launch_linear_timed(c, linear_class(dt, vec, (a).K), linear_bytes(a, dt), dt, !(vec), a,    \
                                   linear_grid((a).n_groups, (a).epi), s);                               \
     if (rc_) return rc_;                                                                                 \
   } while (0)
 
 // Timing class of a linear launch: one per kernel symbol.
-int linear_class(bool vec, int n_groups) {
-  const bool eight = linear_waves(n_groups) == 8;
-  if (vec) return eight ? LEDE_K_LINEAR_VEC8 : LEDE_K_LINEAR_VEC;
-  return eight ? LEDE_K_LINEAR_MFMA8 : LEDE_K_LINEAR_MFMA;
+int linear_class(int dt, bool vec, int K) {
+  switch (linear_x_source(dt, !vec, K)) {
+    case XS_LDS: return LEDE_K_LINEAR_VEC;
+    case XS_GLOBAL: return LEDE_K_LINEAR_VEC_GX;
+    default: return LEDE_K_LINEAR_MFMA;
+  }
 }
 
 #define LAUNCH(cls, bytes, expr)                         \
@@ -318,9 +323,8 @@ int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
 // ---- pass orchestration -----------------------------------------------------------
 
 int linear_grid(int n_groups, int epi) {
-  // one 16-row group per block; the argmax head caps the block count to
-  // bound its atomic updates
-  return epi == EPI_ARGMAX ? std::min(n_groups, 1024) : n_groups;
+  (void)epi;
+  return n_groups;  // one 16-row group per block
 }
 
 // The verify / prefill rows are normalised by the norm kernel (one
@@ -519,6 +523,34 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s) {
   return LEDE_OK;
 }
 
+// Draft passes (k > 0) and the verify pass of a forced step, captured once per
+// (l, k, Q-net layer) into a HIP graph and replayed on the stream.
+int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
+  const auto key = std::make_tuple(l, k, qa);
+  auto it = c->graphs.find(key);
+  if (it == c->graphs.end()) {
+    HIP_CHECK(c, hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal));
+    int rc = k > 0 ? launch_drafts(c, l, 1, k, qa, 0, s) : LEDE_OK;
+    if (!rc) rc = launch_verify(c, k, s);
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(s, &g);
+    if (rc) {
+      if (g) (void)hipGraphDestroy(g);
+      return rc;
+    }
+    if (e != hipSuccess) return fail(c, LEDE_E_HIP, "hipStreamEndCapture: %s", hipGetErrorString(e));
+    hipGraphExec_t ex = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (ei != hipSuccess) return fail(c, LEDE_E_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ei));
+    it = c->graphs.emplace(key, ex).first;
+  }
+  HIP_CHECK(c, hipGraphLaunch(it->second, s));
+  if (k > 0) c->last_draft_rows = k;  // as the eager launches leave them
+  c->last_rows = k + 1;
+  return LEDE_OK;
+}
+
 int read_record(lede_ctx* c, hipStream_t s) {
   HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 48 * 4, hipMemcpyDeviceToHost, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
@@ -598,6 +630,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
 
 void lede_destroy(lede_ctx* c) {
   if (!c) return;
+  for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.second);
   for (hipEvent_t e : c->evpool) (void)hipEventDestroy(e);
   if (c->table_h) (void)hipHostFree(c->table_h);
   if (c->record_h) (void)hipHostFree(c->record_h);
@@ -832,20 +865,34 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
     } else {
       if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
       const int qa = (want_q && l_min <= l) ? l_min : 0;
+      ran_q = qa > 0;
+      if (c->use_graphs && !c->prof && s) {
+        // the whole step as one graph: every launch reads positions, tokens
+        // and pages from device memory, so a capture serves every step of
+        // the same shape
+        if ((rc = step_graph(c, l, k_eff, qa, s))) { truncate_pages(c, c0); return rc; }
+        goto verified;
+      }
       rc = launch_drafts(c, l, 1, k_eff, qa, 0, s);
       if (rc) return rc;
-      ran_q = qa > 0;
     }
   } else {
     k_eff = 0;
     if ((rc = ensure_pages(c, c0 + 1)) || (rc = upload_table(c, s))) return rc;
+    if (forced && c->use_graphs && !c->prof && s) {
+      if ((rc = step_graph(c, l, 0, 0, s))) return rc;
+      goto verified;
+    }
   }
-  if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
-  hipEvent_t ph1 = nullptr;
-  if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
-  rc = launch_verify(c, k_eff, s);
-  if (rc) return rc;
-  if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
+  {
+    if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
+    hipEvent_t ph1 = nullptr;
+    if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
+    rc = launch_verify(c, k_eff, s);
+    if (rc) return rc;
+    if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
+  }
+verified:
   if (ran_q) HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
   rc = read_record(c, s);
   if (rc) return rc;
