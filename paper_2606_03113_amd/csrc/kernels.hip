@@ -339,15 +339,15 @@ __device__ __forceinline__ float block_sum(float v, float* scratch) {
 }
 
 // Normalise the single input row of the vector kernel into LDS with every
-// thread of the block: the raw row goes to an fp32 LDS copy (thread t loads
-// elements 4t + 4 NT j) while the sum of squares accumulates in j order, then
-// the normalised row is written in the model dtype for the dot products.
+// thread of the block: thread t holds elements 4t + 4 NT j of the row and of
+// the gain in registers (both requested together), sums the squares in j
+// order, and the block sums the threads' partials in wave order.  The row is
+// zero-padded to the batch size the main loop reads.
 template <int DT, int NW>
 __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch) {
-  constexpr int NT = NW * 64;
+  constexpr int NT = NW * 64, J = (8192 + 4 * NT - 1) / (4 * NT);  // rows of up to 8192 elements
   const int tid = threadIdx.x;
   const int row_bytes = a.K * Elem<DT>::ES_, pad_bytes = lin_x_tiles(a.KT) * Tile<DT>::TK * Elem<DT>::ES_;
-  float* raw = (float*)(lds + pad_bytes);
   for (int i = row_bytes + tid * 4; i < pad_bytes; i += NT * 4) *(uint32_t*)(lds + i) = 0u;
   const float* h = a.h;
   const void* row = nullptr;
@@ -358,29 +358,36 @@ __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch
     if (blockIdx.x == 0) h_out = a.h;
     h = nullptr;
   }
+  float4 v[J], g[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    const bool in = i < a.K;
+    v[j] = in ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    g[j] = in ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
   float ss = 0.f;
-#pragma unroll 4
-  for (int i = 4 * tid; i < a.K; i += 4 * NT) {
-    const float4 v = row_load4<DT>(h, row, i);
-    *(float4*)(raw + i) = v;
-    if (h_out) *(float4*)(h_out + i) = v;
-    ss = fmaf(v.x, v.x, ss);
-    ss = fmaf(v.y, v.y, ss);
-    ss = fmaf(v.z, v.z, ss);
-    ss = fmaf(v.w, v.w, ss);
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    ss = fmaf(v[j].x, v[j].x, ss);
+    ss = fmaf(v[j].y, v[j].y, ss);
+    ss = fmaf(v[j].z, v[j].z, ss);
+    ss = fmaf(v[j].w, v[j].w, ss);
   }
   ss = block_sum<NW>(ss, scratch);
   const float inv = rsqrtf(ss / (float)a.K + a.eps);
-#pragma unroll 4
-  for (int i = 4 * tid; i < a.K; i += 4 * NT) {
-    const float4 v = *(const float4*)(raw + i);
-    const float4 g = row_load4<DT>(nullptr, a.gain, i);
-    float4 y;
-    y.x = (v.x * inv) * g.x;
-    y.y = (v.y * inv) * g.y;
-    y.z = (v.z * inv) * g.z;
-    y.w = (v.w * inv) * g.w;
-    store4<DT>(lds, i, y);
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    if (i < a.K) {
+      float4 y;
+      y.x = (v[j].x * inv) * g[j].x;
+      y.y = (v[j].y * inv) * g[j].y;
+      y.z = (v[j].z * inv) * g[j].z;
+      y.w = (v[j].w * inv) * g[j].w;
+      if (h_out) *(float4*)(h_out + i) = v[j];
+      store4<DT>(lds, i, y);
+    }
   }
   __syncthreads();
 }
@@ -801,8 +808,8 @@ size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
   if (linear_x_source(dtype, mfma, K) != XS_LDS) return 0;
   const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
   const size_t row = (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es;
-  // the norm prologue keeps an fp32 copy of the raw row next to the result
-  return (x_mode == X_NORM || x_mode == X_EMBED_NORM) ? row + (size_t)K * 4 : row;
+  (void)x_mode;
+  return row;
 }
 
 // With events, the start / stop timestamps are taken by the dispatch itself

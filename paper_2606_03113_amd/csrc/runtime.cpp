@@ -323,8 +323,10 @@ int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
 // ---- pass orchestration -----------------------------------------------------------
 
 int linear_grid(int n_groups, int epi) {
-  (void)epi;
-  return n_groups;  // one 16-row group per block
+  // one 16-row group per block; the argmax head (2000 groups for a 32000-token
+  // vocabulary) runs faster with 1024 blocks taking two groups each than with
+  // 2000 blocks in two waves (46.3 vs 49.9 us measured)
+  return epi == EPI_ARGMAX ? std::min(n_groups, 1024) : n_groups;
 }
 
 // The verify / prefill rows are normalised by the norm kernel (one
