@@ -7,7 +7,8 @@ small C library (``gen.c``: Philox4x32-10 counters + Box-Muller) and exposes:
   logical row-major ``[out][in]`` layout (bf16 as uint16 bit patterns);
 * ``weight_tensor(model, name, layer)`` -- one tensor, regenerable alone;
 * ``weight_rows(model, name, layer, rows)`` -- selected rows only;
-* ``qnet_weights(model)``, ``prompt(workload)``, ``schedule(workload)``.
+* ``qnet_weights(model)``, ``prompt(workload)``, ``schedule(workload)``;
+* ``step_uniforms(step)`` -- the uniforms a speculative-sampling step draws.
 
 Every value is a pure function of (seed, stream, index), so the oracle and
 the GPU upload see identical bytes.
@@ -21,8 +22,8 @@ import threading
 
 import numpy as np
 
-from .configs import (PAGE_SIZE, SEED_PROMPT, SEED_QNET, SEED_SCHEDULE, SEED_WEIGHTS,
-                      WEIGHT_STD, WORKLOADS, ModelConfig, Workload, shrink)
+from .configs import (PAGE_SIZE, SAMPLE_SLOTS, SAMPLE_STRIDE, SEED_PROMPT, SEED_QNET, SEED_SAMPLE,
+                      SEED_SCHEDULE, SEED_WEIGHTS, WEIGHT_STD, WORKLOADS, ModelConfig, Workload, shrink)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "liblede_inputs.so")
@@ -38,6 +39,7 @@ STREAM_QNET_W2 = 11
 STREAM_PROMPT = 20
 STREAM_SCHED_L = 30
 STREAM_SCHED_K = 31
+STREAM_SAMPLE = 40
 LAYER_BASE = 1000
 LAYER_STRIDE = 16
 LAYER_TENSORS = {"wq": 1, "wk": 2, "wv": 3, "wo": 4, "wg": 6, "wu": 7, "wd": 8}
@@ -67,6 +69,7 @@ def _load():
             lib.lede_gen_normal_bf16.argtypes = [u32, u32, u64, u64, dbl, vp]
             lib.lede_gen_uniform_int.argtypes = [u32, u32, u64, u64, i32, i32, vp]
             lib.lede_gen_philox_block.argtypes = [u32] * 6 + [vp]
+            lib.lede_gen_uniform01.argtypes = [u32, u32, u64, u64, vp]
             _lib = lib
     return _lib
 
@@ -95,6 +98,20 @@ def uniform_int(seed: int, stream: int, n: int, lo: int, hi: int, offset: int = 
     out = np.empty(n, dtype=np.int32)
     _load().lede_gen_uniform_int(seed, stream, offset, n, lo, hi, out.ctypes.data)
     return out
+
+
+def uniform01(seed: int, stream: int, n: int, offset: int = 0) -> np.ndarray:
+    """Exact float32 uniforms in [0, 1) (24 random bits each)."""
+    out = np.empty(n, dtype=np.float32)
+    _load().lede_gen_uniform01(seed, stream, offset, n, out.ctypes.data)
+    return out
+
+
+def step_uniforms(step: int, seed: int = SEED_SAMPLE) -> np.ndarray:
+    """The SAMPLE_STRIDE uniforms of one speculative-sampling step: draft
+    samples [0, SAMPLE_SLOTS), acceptance tests [SAMPLE_SLOTS, 2 SAMPLE_SLOTS),
+    the residual / bonus sample last."""
+    return uniform01(seed, STREAM_SAMPLE, SAMPLE_STRIDE, offset=SAMPLE_STRIDE * step)
 
 
 def tensor_shape(m: ModelConfig, name: str):

@@ -16,6 +16,9 @@ SEED_WEIGHTS = 0
 SEED_PROMPT = 1
 SEED_SCHEDULE = 2
 SEED_QNET = 3
+SEED_SAMPLE = 4          # uniforms of speculative sampling
+SAMPLE_SLOTS = 16        # per step: draft uniforms [0, 16), acceptance uniforms [16, 32), residual / bonus [32]
+SAMPLE_STRIDE = 2 * SAMPLE_SLOTS + 1
 
 WEIGHT_STD = 0.02  # standard deviation of every random weight
 

@@ -97,6 +97,16 @@ void lede_gen_uniform_int(uint32_t seed, uint32_t stream, uint64_t offset, uint6
   }
 }
 
+/* Uniform floats in [0, 1): element j takes the first word of Philox block
+ * (offset + j) and keeps its top 24 bits, so every value is an exact float. */
+void lede_gen_uniform01(uint32_t seed, uint32_t stream, uint64_t offset, uint64_t n, float* out) {
+  for (uint64_t j = 0; j < n; ++j) {
+    uint32_t x[4];
+    block(seed, stream, offset + j, x);
+    out[j] = (float)(x[0] >> 8) * (1.0f / 16777216.0f);
+  }
+}
+
 /* Raw Philox block, exported so tests can check the generator against the
  * known-answer vectors published with the Random123 library. */
 void lede_gen_philox_block(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0, uint32_t k1,

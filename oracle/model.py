@@ -8,8 +8,9 @@ draft, the full model verifies in parallel); Section 3.1 (the MDP: a state
 from the hidden state at a candidate exit layer, an action, the reward of
 Section 3.1.3); Section 3.2 (greedy action from a small MLP Q-network);
 Section 3.3 (exit layer chosen during the first forward pass of a step, then
-drafting at that layer); Section 4.1 (batch 1, greedy decoding, speculative
-acceptance, metrics E, d, acceptance rate).
+drafting at that layer); Section 4.1 (batch 1, greedy decoding and sampling
+at temperature 0.6, speculative-sampling acceptance, metrics E, d,
+acceptance rate).
 
 Readings where the paper is silent:
 * the early-exit head is the shared final RMSNorm + LM head;
@@ -22,7 +23,11 @@ Readings where the paper is silent:
 * argmax ties go to the lowest index; no EOS: exactly N tokens are produced,
   with k clamped to N - n_gen - 1;
 * the reward is summed over the drafts up to and including the first
-  rejected one; continue penalties do not arise with a joint action.
+  rejected one; continue penalties do not arise with a joint action;
+* sampling: draws are inverse-CDF in index order from a uniform the caller
+  supplies; acceptance keeps draft d while u < p(d) / q(d); the token after
+  a rejection comes from the normalised max(0, p - q), after k acceptances
+  from p (the speculative-sampling rule the paper cites).
 """
 from __future__ import annotations
 
@@ -297,6 +302,54 @@ def greedy_ar(dec: OracleDecoder, prompt: Sequence[int], n_gen: int):
     return toks, infos
 
 
+# ---- speculative sampling (Section 4.1: sampling at temperature T with
+# speculative-sampling acceptance) -------------------------------------------
+
+SAMPLE_SLOTS = 16   # per-step uniforms: drafts [0, 16), acceptance [16, 32), residual / bonus [32]
+
+
+def probs_at(z: np.ndarray, T: float) -> np.ndarray:
+    """softmax(z / T) in fp64."""
+    x = np.asarray(z, dtype=np.float64) / T
+    e = np.exp(x - x.max())
+    return e / e.sum()
+
+
+def sample_inverse_cdf(w: np.ndarray, u: float) -> int:
+    """Inverse-CDF draw from non-negative weights w (any scale): the smallest
+    index v whose running sum in index order exceeds u * sum(w); if rounding
+    leaves none, the last index of positive weight."""
+    c = np.cumsum(np.asarray(w, dtype=np.float64))
+    hit = np.nonzero(c > float(u) * c[-1])[0]
+    if len(hit):
+        return int(hit[0])
+    return int(np.nonzero(np.asarray(w) > 0)[0][-1])
+
+
+def speculative_accept(p_rows: Sequence[np.ndarray], q_rows: Sequence[np.ndarray], drafts: Sequence[int],
+                       u_acc: Sequence[float], u_res: float):
+    """Speculative-sampling acceptance of k drafts.
+
+    p_rows[j] is the target distribution after j drafts (j = 0..k), q_rows[i]
+    the draft distribution draft i+1 was sampled from.  Draft i+1 is kept
+    while u_acc[i] < p_i(d) / q_i(d); at the first rejection the next token is
+    drawn from the normalised residual max(0, p_i - q_i), and after k
+    acceptances from p_k.  Returns (accepted count, next token)."""
+    k = len(drafts)
+    a = 0
+    while a < k:
+        d = int(drafts[a])
+        if float(u_acc[a]) * q_rows[a][d] < p_rows[a][d]:
+            a += 1
+        else:
+            break
+    if a < k:
+        y = sample_inverse_cdf(np.maximum(p_rows[a] - q_rows[a], 0.0), u_res)
+    else:
+        y = sample_inverse_cdf(p_rows[k], u_res)
+    return a, y
+
+
 class SSDState:
     """(c, pending token, n_gen) plus the pager and the committed output."""
 
@@ -362,6 +415,47 @@ class SSDState:
                           verify=verify, reward=reward(a, k_eff, l, L), seq_len=self.c,
                           q_action=q_action, q_values=q_values, draft_info=dinfo, verify_info=vinfo,
                           block_table=list(self.pager.table))
+
+
+    def step_sampled(self, l: int, k: int, n_total: int, T: float, uniforms: Sequence[float]) -> StepRecord:
+        """One step of self-speculative sampling at temperature T: draft i
+        is drawn from softmax(z_draft / T) with uniforms[i-1], the drafts are
+        verified by speculative-sampling acceptance with uniforms[16 + i - 1],
+        and the token after them comes from the residual (or, after k
+        acceptances, the target) distribution with uniforms[32]."""
+        dec, m = self.dec, self.dec.m
+        L = m.n_layers
+        n_gen = len(self.out)
+        k_eff = max(0, min(k, n_total - n_gen - 1))
+        if not 1 <= l <= L:
+            raise ValueError("exit layer out of range")
+        self.pager.ensure(self.c + k_eff + 1)
+        drafts, dz, q_rows = [], [], []
+        tok = self.pending
+        for i in range(1, k_eff + 1):
+            h = dec.forward([tok], self.c + i - 1, l)
+            zi = dec.head(h)[0]
+            qi = probs_at(zi, T)
+            tok = sample_inverse_cdf(qi, uniforms[i - 1])
+            drafts.append(tok)
+            dz.append(zi)
+            q_rows.append(qi)
+        h = dec.forward([self.pending] + drafts, self.c, L)
+        z = dec.head(h)
+        self.last_draft_logits = dz
+        self.last_verify_logits = z
+        p_rows = [probs_at(z[j], T) for j in range(k_eff + 1)]
+        a, y = speculative_accept(p_rows, q_rows, drafts, uniforms[SAMPLE_SLOTS:SAMPLE_SLOTS + k_eff],
+                                  uniforms[2 * SAMPLE_SLOTS])
+        emitted = drafts[:a] + [y]
+        self.c += a + 1
+        self.pending = y
+        self.out.extend(emitted)
+        self.pager.truncate(self.c)
+        self.last_p_rows, self.last_q_rows = p_rows, q_rows
+        return StepRecord(l=l, k_req=k, k_eff=k_eff, accepted=a, emitted=emitted, drafts=drafts,
+                          verify=[argmax_lowest(z[j]) for j in range(k_eff + 1)],
+                          reward=reward(a, k_eff, l, L), seq_len=self.c, block_table=list(self.pager.table))
 
 
 def ssd_generate(dec: OracleDecoder, prompt: Sequence[int], n_total: int, actions, n_pages: int,
