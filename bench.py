@@ -112,6 +112,8 @@ def main():
     ap.add_argument("--prof-steps", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graphs", type=int, default=0)
+    ap.add_argument("--temperature", type=float, default=0.0,
+                    help="> 0: speculative sampling at this temperature (uniforms from the seeded generator)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, copy this many MiB device-to-device three times (a kernel of "
                          "known traffic for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -163,11 +165,20 @@ def main():
     produced = [first]
     log_q = m.qnet_hidden > 0
 
+    n_steps = [0]
+
     def step():
-        rec = eng.lede_step((l, k), n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
+        if args.temperature > 0:
+            rec = eng.lede_step_sampled((l, k), args.temperature, li.step_uniforms(n_steps[0]),
+                                        n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
+        else:
+            rec = eng.lede_step((l, k), n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
+        n_steps[0] += 1
         produced.extend(rec.emitted)
         return rec
 
+    if args.graphs and args.temperature > 0:
+        sys.exit("sampled steps are not captured in graphs")
     if args.warmup + args.steps >= wl.n_gen - 1:
         sys.exit("warmup + steps must stay below the %d generated tokens" % wl.n_gen)
     for _ in range(args.warmup):
@@ -194,6 +205,7 @@ def main():
         eng.lede_truncate(wl.prompt_len)
         eng.lede_set_pending(first)
         del produced[1:]
+        n_steps[0] = 0
         for _ in range(min(args.warmup, 3)):
             step()
         eng.lede_prof_enable(level)
@@ -212,11 +224,16 @@ def main():
     eng.lede_set_pending(first)
     del produced[1:]
     n_ar = min(args.steps, wl.n_gen - 2)
-    for _ in range(min(args.warmup, 3)):
-        eng.lede_step((l, 0), log_qnet=False)
+    def ar_step(i):
+        if args.temperature > 0:
+            return eng.lede_step_sampled((l, 0), args.temperature, li.step_uniforms(i), log_qnet=False)
+        return eng.lede_step((l, 0), log_qnet=False)
+
+    for i in range(min(args.warmup, 3)):
+        ar_step(i)
     torch.cuda.synchronize()
     e0.record(stream)
-    ar_recs = [eng.lede_step((l, 0), log_qnet=False) for _ in range(n_ar)]
+    ar_recs = [ar_step(i) for i in range(n_ar)]
     e1.record(stream)
     torch.cuda.synchronize()
     ar_ms = e0.elapsed_time(e1)
@@ -247,8 +264,9 @@ def main():
     accepted = sum(r.accepted for r in recs)
     drafted = sum(r.k_eff for r in recs)
     out = {
-        "metric": "decode tokens/s (batch 1, SSD) + % of HBM peak, Llama-2-7B-shaped bf16"
-        if wl.name == "llama2-7b" else "decode tokens/s (batch 1, SSD), %s" % wl.name,
+        "metric": ("decode tokens/s (batch 1, SSD) + % of HBM peak, Llama-2-7B-shaped bf16"
+                   if wl.name == "llama2-7b" else "decode tokens/s (batch 1, SSD), %s" % wl.name)
+        + (", speculative sampling T=%g" % args.temperature if args.temperature > 0 else ""),
         "value": round(acc_tokens / (ms / 1e3), 3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -265,7 +283,9 @@ def main():
                                (m.name, m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.ffn_dim, m.vocab,
                                 wl.prompt_len, wl.n_gen, l, k),
                    "batch": 1, "prompt_len": wl.prompt_len, "exit_layer": l, "draft_len": k,
-                   "graphs": bool(args.graphs)},
+                   "graphs": bool(args.graphs),
+                   "acceptance": ("speculative sampling, T=%g" % args.temperature if args.temperature > 0
+                                  else "greedy")},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": kname,
                      "avg_launch_us": round(1e3 * d["ms"] / max(d["launches"], 1), 3),

@@ -182,13 +182,34 @@ int lede_verify(lede_ctx* ctx, void* stream, int32_t* accepted, int32_t* tokens,
 int lede_step(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
               void* stream, lede_step_record* rec);
 
+/* ---- speculative sampling (Section 4.1: sampling at temperature T, e.g.
+ * 0.6, with speculative-sampling acceptance) -------------------------------
+ * A step as lede_step, except that
+ *  - draft i is drawn from softmax(z_draft / T) by inverse CDF in index
+ *    order with uniforms[i-1];
+ *  - draft i is kept while uniforms[16 + i - 1] * q(d) < p(d), q the draft
+ *    distribution and p the full model's at that position;
+ *  - the token after the kept drafts is drawn (uniforms[32]) from the
+ *    normalised residual max(0, p - q) at the first rejection, else from p
+ *    after the last draft.
+ * uniforms: host pointer to LEDE_SAMPLE_STRIDE floats, each in [0, 1); the
+ * caller owns the random numbers, so a step is a pure function of its
+ * inputs.  temperature must be finite and > 0 (LEDE_E_ARG otherwise, state
+ * unchanged).  rec->drafts holds the drawn drafts.  Not captured in graphs.
+ * Synchronises as lede_step. */
+#define LEDE_SAMPLE_SLOTS 16
+#define LEDE_SAMPLE_STRIDE 33
+int lede_step_sampled(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
+                      float temperature, const float* uniforms, void* stream, lede_step_record* rec);
+
 /* Committed KV length, pending token and the page table (host copies). */
 int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t* block_table,
                       int32_t cap, int32_t* n_table);
 
 /* Debug read-back (needs set_options(debug=1)); which = 0: logits of the
- * last head launch [rows][vocab] fp32; 1: Q-values of the last Q-network
- * run [E*K]; 2: the Q-network's input state [d] fp32.  *rows receives the
+ * last verify / prefill head launch [rows][vocab] fp32; 1: Q-values of the
+ * last Q-network run [E*K]; 2: the Q-network's input state [d] fp32; 3:
+ * logits of the last step's draft heads [rows][vocab].  *rows receives the
  * row count.  Synchronises. */
 int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows,
                     void* stream);
@@ -237,6 +258,14 @@ int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* t
  * matrix-core kernel of the verify path. */
 int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M,
                    float* y, int32_t use_mfma, void* stream);
+
+/* One draw from softmax(logits / temperature) by inverse CDF in index order
+ * with the uniform u in [0, 1), as the sampled step draws its drafts: logits
+ * is a device fp32 row of V, *token (host) receives the index.  Allocates a
+ * 16-byte device buffer and synchronises (a test and tooling entry point).
+ * LEDE_E_ARG on a null pointer, V < 1, temperature not finite and > 0, or u
+ * outside [0, 1). */
+int lede_op_sample(const float* logits, int32_t V, float temperature, float u, int32_t* token, void* stream);
 
 /* Achievable HBM read bandwidth: reads `bytes` (a multiple of 16, > 0) of the
  * device buffer src once, with the same non-temporal 16-byte loads the

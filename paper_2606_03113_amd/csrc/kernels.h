@@ -140,6 +140,27 @@ struct AcceptArgs {
   int32_t* record;         // [0] a, [1] n_emitted, [2] seq_len, [3] pending, [4..] tokens, [24..] drafts
 };
 
+// Speculative sampling at temperature T (inv_t = 1 / T).  Draft and verify
+// logits are fp32 rows of `vocab`; stats rows hold (max logit, sum of
+// exp((z - max) * inv_t)).  Uniforms per step: drafts [0, 16), acceptance
+// tests [16, 32), residual / bonus draw [32].
+constexpr int SAMPLE_SLOTS = 16;
+struct SampleArgs {
+  const float* logits; int vocab; float inv_t;
+  const float* u; int u_index;   // the draw uses u[u_index] (u_imm when u is null)
+  float u_imm;
+  uint64_t* key_out;             // argmax-style key of the drawn token
+  float* stats_out;              // (max, sum) of the row
+};
+struct SampledAcceptArgs {
+  AcceptArgs acc;                // keys, k, commit targets
+  const float* dlogits;          // [k][vocab] draft rows (row i drew draft i+1)
+  const float* dstats;           // [k][2]
+  const float* vlogits;          // [k+1][vocab]
+  int vocab; float inv_t;
+  const float* u;                // the step's uniforms
+};
+
 // Launchers (kernels.hip).  All return hipError_t of the launch.
 hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s);
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s);
@@ -149,6 +170,8 @@ hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hi
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s);
 hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s);
 hipError_t launch_accept(const AcceptArgs& a, hipStream_t s);
+hipError_t launch_sample(const SampleArgs& a, hipStream_t s);
+hipError_t launch_accept_sampled(const SampledAcceptArgs& a, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
 // Reads bytes (a multiple of 16) of src once; e0 / e1 (may be null) bracket
 // the kernel's execution.

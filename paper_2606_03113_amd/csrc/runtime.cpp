@@ -23,6 +23,7 @@ namespace {
 constexpr int PAGE = 64;
 constexpr int MROWS = 16;   // rows of one verify / prefill pass
 constexpr int RECORD_INTS = 64;
+constexpr int UNIF_FLOATS = 2 * SAMPLE_SLOTS + 1;  // uniforms of a sampled step
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -35,7 +36,7 @@ struct Layout {
   size_t embed, final_norm, head, qw1, qb1, qw2, qb2, wbytes;
   // workspace offsets
   size_t h, xn, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
-      record, rope, wsbytes;
+      record, rope, unif, dstats, wsbytes;
   size_t kvbytes, kv_half;
 };
 
@@ -117,6 +118,8 @@ Layout make_layout(const lede_config* c) {
   o.prompt = take((size_t)o.max_ctx * 4);
   o.record = take(RECORD_INTS * 4);
   o.rope = take((size_t)o.max_ctx * (o.hd / 2) * 8);
+  o.unif = take(UNIF_FLOATS * 4);
+  o.dstats = take(2 * SAMPLE_SLOTS * 4);
   o.wsbytes = off;
 
   o.kv_half = align256((size_t)o.L * o.n_pages * o.nkv * PAGE * o.hd * o.es);
@@ -140,6 +143,7 @@ struct lede_ctx {
   std::vector<int32_t> table;
   int32_t* table_h = nullptr;   // pinned mirror uploaded to the device table
   int32_t* record_h = nullptr;  // pinned read-back of the step record
+  float* unif_h = nullptr;      // pinned staging of a sampled step's uniforms
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
@@ -485,34 +489,49 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   return LEDE_OK;
 }
 
-float* draft_logits(lede_ctx* c, int i) {
-  return c->debug ? c->S<float>(c->lo.logits) + (size_t)(MROWS + i) * c->lo.V : nullptr;
+// Logits rows in the workspace: verify / prefill rows first, draft rows after
+// them.  Greedy steps write them only in debug mode; sampled steps always.
+float* draft_logits(lede_ctx* c, int i, bool always = false) {
+  return (c->debug || always) ? c->S<float>(c->lo.logits) + (size_t)(MROWS + i) * c->lo.V : nullptr;
 }
-float* verify_logits(lede_ctx* c) { return c->debug ? c->S<float>(c->lo.logits) : nullptr; }
+float* verify_logits(lede_ctx* c, bool always = false) {
+  return (c->debug || always) ? c->S<float>(c->lo.logits) : nullptr;
+}
 
 // Draft passes i = i0..k (1-based): token i-1 -> layers [0, l) -> head -> key i.
-// qnet_after applies to pass 1 only.
-int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_begin, hipStream_t s) {
+// qnet_after applies to pass 1 only.  inv_t > 0: draft i is drawn from
+// softmax(z / T) with the step's uniform i-1 instead of taken as the argmax.
+int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_begin, hipStream_t s,
+                  float inv_t = 0.f) {
   uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
+  const bool sampled = inv_t > 0.f;
   for (int i = i0; i <= k; ++i) {
     TokenSrc tok{nullptr, dk + (i - 1)};
     const int begin = i == 1 ? pass1_begin : 0;
     int rc = run_layers(c, 1, true, tok, i - 1, begin, l, i == 1 ? qnet_after : 0, dk + i, s);
     if (rc) return rc;
-    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1), s);
+    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1, sampled), s);
     if (rc) return rc;
+    if (sampled) {
+      SampleArgs sa{};
+      sa.logits = draft_logits(c, i - 1, true); sa.vocab = c->lo.V; sa.inv_t = inv_t;
+      sa.u = c->S<float>(c->lo.unif); sa.u_index = i - 1;
+      sa.key_out = dk + i; sa.stats_out = c->S<float>(c->lo.dstats) + 2 * (i - 1);
+      LAUNCH(LEDE_K_ACCEPT, (double)c->lo.V * 4, launch_sample(sa, s));
+    }
   }
   c->last_draft_rows = k;
   return LEDE_OK;
 }
 
-int launch_verify(lede_ctx* c, int k, hipStream_t s) {
+int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f) {
   uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
   uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
+  const bool sampled = inv_t > 0.f;
   TokenSrc tok{nullptr, dk};
   int rc = run_layers(c, k + 1, false, tok, 0, 0, c->lo.L, 0, vk, s);
   if (rc) return rc;
-  rc = run_head(c, k + 1, false, vk, verify_logits(c), s);
+  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled), s);
   if (rc) return rc;
   AcceptArgs aa{};
   aa.dkeys = dk; aa.vkeys = vk; aa.k = k;
@@ -520,7 +539,17 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s) {
   aa.block_table = c->S<int32_t>(c->lo.btab);
   aa.pending_out = dk;
   aa.record = c->S<int32_t>(c->lo.record);
-  LAUNCH(LEDE_K_ACCEPT, 256.0, launch_accept(aa, s));
+  if (sampled) {
+    SampledAcceptArgs sa{};
+    sa.acc = aa;
+    sa.dlogits = draft_logits(c, 0, true); sa.dstats = c->S<float>(c->lo.dstats);
+    sa.vlogits = verify_logits(c, true);
+    sa.vocab = c->lo.V; sa.inv_t = inv_t;
+    sa.u = c->S<float>(c->lo.unif);
+    LAUNCH(LEDE_K_ACCEPT, (double)(2 * k + 1) * c->lo.V * 4, launch_accept_sampled(sa, s));
+  } else {
+    LAUNCH(LEDE_K_ACCEPT, 256.0, launch_accept(aa, s));
+  }
   c->last_rows = k + 1;
   return LEDE_OK;
 }
@@ -603,6 +632,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
   for (int i = 0; i < o.n_pages; ++i) c->free_list.push_back(i);
   if (hipHostMalloc((void**)&c->table_h, (size_t)o.max_pages_seq * 4 + 256, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->record_h, RECORD_INTS * 4, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->unif_h, UNIF_FLOATS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->keys_h, 32 * 8, 0) != hipSuccess) {
     lede_destroy(c);
     return LEDE_E_HIP;
@@ -636,6 +666,7 @@ void lede_destroy(lede_ctx* c) {
   for (hipEvent_t e : c->evpool) (void)hipEventDestroy(e);
   if (c->table_h) (void)hipHostFree(c->table_h);
   if (c->record_h) (void)hipHostFree(c->record_h);
+  if (c->unif_h) (void)hipHostFree(c->unif_h);
   if (c->keys_h) (void)hipHostFree(c->keys_h);
   delete c;
 }
@@ -819,14 +850,28 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
   return LEDE_OK;
 }
 
-int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, void* stream,
-              lede_step_record* rec) {
+}  // extern "C"
+
+namespace {
+
+// One step (greedy when temperature == 0, speculative sampling otherwise).
+int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, float temperature,
+              const float* uniforms, void* stream, lede_step_record* rec) {
   if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
   if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
   const Layout& o = c->lo;
   if (!forced && !o.H) return fail(c, LEDE_E_STATE, "no Q-network configured");
+  const bool sampled = temperature != 0.f;
+  if (sampled) {
+    if (!(temperature > 0.f) || !std::isfinite(temperature))
+      return fail(c, LEDE_E_ARG, "temperature must be finite and > 0");
+    if (!uniforms) return fail(c, LEDE_E_ARG, "null uniforms");
+    for (int i = 0; i < UNIF_FLOATS; ++i)
+      if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return fail(c, LEDE_E_ARG, "uniform %d not in [0, 1)", i);
+  }
+  const float inv_t = sampled ? 1.f / temperature : 0.f;
   hipStream_t s = S_(stream);
   int rc0 = 0;
   memset(rec, 0, sizeof *rec);
@@ -836,6 +881,10 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   if (forced) {
     if (l < 1 || l > o.L) return fail(c, LEDE_E_ARG, "exit layer %d not in 1..%d", l, o.L);
     if (k < 0 || k > o.k_max) return fail(c, LEDE_E_ARG, "draft length %d not in 0..%d", k, o.k_max);
+  }
+  if (sampled) {
+    memcpy(c->unif_h, uniforms, UNIF_FLOATS * 4);
+    HIP_CHECK(c, hipMemcpyAsync(c->S<float>(o.unif), c->unif_h, UNIF_FLOATS * 4, hipMemcpyHostToDevice, s));
   }
   const int l_min = o.H ? c->cfg.exits[0] : 0;
   const bool want_q = o.H && (!forced || log_qnet);
@@ -862,26 +911,26 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       k_eff = std::min(std::min(k, o.k_max), n_remaining - 1);
       ran_q = true;
       if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
-      rc = launch_drafts(c, l, 1, k_eff, 0, l_min, s);
+      rc = launch_drafts(c, l, 1, k_eff, 0, l_min, s, inv_t);
       if (rc) return rc;
     } else {
       if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
       const int qa = (want_q && l_min <= l) ? l_min : 0;
       ran_q = qa > 0;
-      if (c->use_graphs && !c->prof && s) {
+      if (c->use_graphs && !c->prof && s && !sampled) {
         // the whole step as one graph: every launch reads positions, tokens
         // and pages from device memory, so a capture serves every step of
         // the same shape
         if ((rc = step_graph(c, l, k_eff, qa, s))) { truncate_pages(c, c0); return rc; }
         goto verified;
       }
-      rc = launch_drafts(c, l, 1, k_eff, qa, 0, s);
+      rc = launch_drafts(c, l, 1, k_eff, qa, 0, s, inv_t);
       if (rc) return rc;
     }
   } else {
     k_eff = 0;
     if ((rc = ensure_pages(c, c0 + 1)) || (rc = upload_table(c, s))) return rc;
-    if (forced && c->use_graphs && !c->prof && s) {
+    if (forced && c->use_graphs && !c->prof && s && !sampled) {
       if ((rc = step_graph(c, l, 0, 0, s))) return rc;
       goto verified;
     }
@@ -890,7 +939,7 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
     if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
     hipEvent_t ph1 = nullptr;
     if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
-    rc = launch_verify(c, k_eff, s);
+    rc = launch_verify(c, k_eff, s, inv_t);
     if (rc) return rc;
     if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
   }
@@ -923,6 +972,40 @@ verified:
     rec->reward = (float)(a * (1.0 + lam) + (a < k_eff ? (-2.0 + lam) : 0.0));
   }
   return LEDE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, void* stream,
+              lede_step_record* rec) {
+  return step_impl(c, forced, log_qnet, n_remaining, 0.f, nullptr, stream, rec);
+}
+
+int lede_step_sampled(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
+                      float temperature, const float* uniforms, void* stream, lede_step_record* rec) {
+  if (c && !(temperature > 0.f)) return fail(c, LEDE_E_ARG, "temperature must be > 0");
+  return step_impl(c, forced, log_qnet, n_remaining, temperature, uniforms, stream, rec);
+}
+
+int lede_op_sample(const float* logits, int32_t V, float temperature, float u, int32_t* token, void* stream) {
+  if (!logits || !token || V < 1) return LEDE_E_ARG;
+  if (!(temperature > 0.f) || !std::isfinite(temperature) || !(u >= 0.f && u < 1.f)) return LEDE_E_ARG;
+  hipStream_t s = S_(stream);
+  uint64_t* key = nullptr;
+  if (hipMalloc((void**)&key, 16) != hipSuccess) return LEDE_E_HIP;
+  SampleArgs sa{};
+  sa.logits = logits; sa.vocab = V; sa.inv_t = 1.f / temperature;
+  sa.u = nullptr; sa.u_imm = u; sa.key_out = key; sa.stats_out = nullptr;
+  uint64_t h = 0;
+  int rc = LEDE_OK;
+  if (launch_sample(sa, s) != hipSuccess || hipMemcpyAsync(&h, key, 8, hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    rc = LEDE_E_HIP;
+  (void)hipFree(key);
+  if (rc == LEDE_OK) *token = (int32_t)(0xFFFFFFFFu - (uint32_t)(h & 0xFFFFFFFFull));
+  return rc;
 }
 
 int lede_get_kv_state(lede_ctx* c, int32_t* seq_len, int32_t* pending, int32_t* bt, int32_t cap, int32_t* n_table) {

@@ -65,7 +65,9 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
             "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
-            "lede_op_read_probe"]
+            "lede_op_read_probe", "lede_step_sampled", "lede_op_sample"]
+SAMPLE_SLOTS = 16
+SAMPLE_STRIDE = 33
 
 _lib = None
 
@@ -104,6 +106,9 @@ def load(path: str = LIB_PATH):
     L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
     L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, vp, i32, vp]
     L.lede_op_read_probe.argtypes = [vp, sz, vp, i32, vp, P(ctypes.c_float)]
+    L.lede_step_sampled.argtypes = [vp, P(LedeAction), i32, i32, ctypes.c_float, P(ctypes.c_float), vp,
+                                    P(LedeStepRecord)]
+    L.lede_op_sample.argtypes = [vp, i32, ctypes.c_float, ctypes.c_float, P(i32), vp]
     for name in EXPORTED:
         if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes"):
             getattr(L, name).restype = ctypes.c_int
@@ -256,15 +261,33 @@ class Engine:
                                        _i32p(ver)), self.ctx)
         return acc.value, [int(x) for x in toks[:ne.value]], ver
 
+    @staticmethod
+    def _record(rec) -> StepRecord:
+        return StepRecord(l=rec.l, k_req=rec.k_req, k_eff=rec.k_eff, accepted=rec.accepted,
+                          emitted=[rec.tokens[i] for i in range(rec.n_emitted)],
+                          drafts=[rec.drafts[i] for i in range(rec.k_eff)], q_action=rec.q_action,
+                          q_max=rec.q_max, reward=rec.reward, seq_len=rec.seq_len, pending=rec.pending)
+
     def lede_step(self, action=None, n_remaining: int = 1 << 30, log_qnet: bool = True) -> StepRecord:
         rec = LedeStepRecord()
         act = LedeAction(int(action[0]), int(action[1])) if action is not None else None
         self._check(self.L.lede_step(self.ctx, ctypes.byref(act) if act is not None else None, int(log_qnet),
                                      int(n_remaining), self.stream, ctypes.byref(rec)), self.ctx)
-        return StepRecord(l=rec.l, k_req=rec.k_req, k_eff=rec.k_eff, accepted=rec.accepted,
-                          emitted=[rec.tokens[i] for i in range(rec.n_emitted)],
-                          drafts=[rec.drafts[i] for i in range(rec.k_eff)], q_action=rec.q_action,
-                          q_max=rec.q_max, reward=rec.reward, seq_len=rec.seq_len, pending=rec.pending)
+        return self._record(rec)
+
+    def lede_step_sampled(self, action, temperature: float, uniforms, n_remaining: int = 1 << 30,
+                          log_qnet: bool = True) -> StepRecord:
+        """A speculative-sampling step; uniforms: SAMPLE_STRIDE floats in [0, 1)."""
+        rec = LedeStepRecord()
+        act = LedeAction(int(action[0]), int(action[1])) if action is not None else None
+        u = np.ascontiguousarray(uniforms, dtype=np.float32)
+        if u.size != SAMPLE_STRIDE:
+            raise ValueError("need %d uniforms" % SAMPLE_STRIDE)
+        self._check(self.L.lede_step_sampled(self.ctx, ctypes.byref(act) if act is not None else None,
+                                             int(log_qnet), int(n_remaining), float(temperature),
+                                             u.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), self.stream,
+                                             ctypes.byref(rec)), self.ctx)
+        return self._record(rec)
 
     def lede_get_kv_state(self):
         """(seq_len, pending, block table)."""
@@ -337,3 +360,17 @@ def op_read_probe(buf, grid: int = 0) -> float:
     if rc:
         raise LedeError(rc, "op_read_probe")
     return ms.value
+
+
+def op_sample(logits, temperature: float, u: float) -> int:
+    """One inverse-CDF draw from softmax(logits / temperature) by the
+    library's sampling kernel; logits is a float32 GPU tensor of one row."""
+    import torch
+    L = load()
+    tok = ctypes.c_int32()
+    s = ctypes.c_void_p(torch.cuda.current_stream(logits.device).cuda_stream)
+    x = logits.contiguous()
+    rc = L.lede_op_sample(x.data_ptr(), x.numel(), float(temperature), float(u), ctypes.byref(tok), s)
+    if rc:
+        raise LedeError(rc, "op_sample")
+    return tok.value

@@ -15,6 +15,7 @@ from typing import List
 
 import numpy as np
 
+from oracle import model as om
 from oracle.model import OracleDecoder, SSDState, Tolerance
 
 TOL = Tolerance()
@@ -148,6 +149,115 @@ def check_ssd(eng, st: SSDState, model, n_total, actions, rep: Report, qnet_log=
             assert table == orc.block_table, (table, orc.block_table)
             assert abs(rec.reward - orc.reward) < 1e-5
         else:
+            eng.lede_truncate(c0)
+            eng.lede_prefill([pending0] + orc.emitted[:-1])
+            eng.lede_set_pending(st.pending)
+            sl, pend, table = eng.lede_get_kv_state()
+            assert (sl, pend) == (st.c, st.pending)
+            assert table == orc.block_table
+    return rep
+
+
+# ---- speculative sampling -------------------------------------------------------
+
+CDF_EPS = 2e-5   # fp32 running sums against the fp64 CDF
+
+
+def _cdf_interval(w, v):
+    c = np.cumsum(np.asarray(w, dtype=np.float64))
+    c = c / c[-1]
+    return (c[v - 1] if v > 0 else 0.0), c[v]
+
+
+def draw_consistent(w, v, u, delta):
+    """v is an inverse-CDF draw of u from weights w up to delta in the CDF."""
+    if v < 0 or v >= len(w) or w[v] <= 0:
+        return False
+    lo, hi = _cdf_interval(w, v)
+    return lo - delta <= u <= hi + delta
+
+
+def _spread(eps, T):
+    """Bound on how far a CDF or a probability ratio moves when every logit
+    moves by at most eps (softmax at temperature T)."""
+    return 2.0 * (np.exp(2.0 * eps / T) - 1.0) + CDF_EPS
+
+
+def _decisions(zd, zv, drafts, u, T):
+    """The acceptance count and the draw weights of the token after it, from
+    one set of logits (rows of drafts, rows of verify)."""
+    k = len(drafts)
+    p = [om.probs_at(zv[j], T) for j in range(k + 1)]
+    q = [om.probs_at(zd[i], T) for i in range(k)]
+    a = 0
+    while a < k and u[om.SAMPLE_SLOTS + a] * q[a][drafts[a]] < p[a][drafts[a]]:
+        a += 1
+    w = np.maximum(p[a] - q[a], 0.0) if a < k else p[a]
+    return a, w, p, q
+
+
+def check_sampled(eng, st: SSDState, model, n_total, actions, T, rep: Report, step0=0):
+    """Self-speculative sampling on the GPU against the oracle, step by step,
+    with the same uniforms.  Every GPU decision must follow the rule on the
+    GPU's own logits (to fp32 rounding); it must equal the oracle's decision
+    unless the oracle's margin is within what the logit tolerance allows (a
+    near-tie substitution, after which the GPU is resynchronised onto the
+    oracle's committed state).  Integers are bit-exact otherwise."""
+    import lede_inputs as li
+    dt = model.dtype
+    i = 0
+    while len(st.out) < n_total:
+        l, k = actions[i % len(actions)]
+        u = li.step_uniforms(step0 + i)
+        i += 1
+        c0, pending0 = st.c, st.pending
+        n_rem = n_total - len(st.out)
+        orc = st.step_sampled(int(l), int(k), n_total, T, u)
+        rec = eng.lede_step_sampled((int(l), int(k)), T, u, n_remaining=n_rem)
+        rep.steps += 1
+        assert rec.k_eff == orc.k_eff
+        ke = orc.k_eff
+        zd = eng.logits(3)[:ke] if ke else np.zeros((0, model.vocab))
+        zv = eng.logits(0)
+        assert len(zv) == ke + 1
+        diverged = False
+        eps = 0.0
+        # drafts: each row compared while the token histories agree
+        for j in range(ke):
+            rep.row(dt, zd[j], st.last_draft_logits[j])
+            eps = max(eps, float(np.max(np.abs(zd[j] - st.last_draft_logits[j]))))
+            g = rec.drafts[j]
+            assert draw_consistent(om.probs_at(zd[j], T), g, u[j], CDF_EPS), ("draft draw", j)
+            if g != orc.drafts[j]:
+                assert draw_consistent(st.last_q_rows[j], g, u[j], _spread(eps, T)), ("draft", j)
+                diverged = True
+                break
+        if not diverged:
+            for j in range(ke + 1):
+                rep.row(dt, zv[j], st.last_verify_logits[j])
+                eps = max(eps, float(np.max(np.abs(zv[j] - st.last_verify_logits[j]))))
+            a_g, w_g, _, _ = _decisions(zd, zv, rec.drafts, u, T)
+            assert a_g == rec.accepted, ("acceptance on the GPU's own logits", a_g, rec.accepted)
+            assert draw_consistent(w_g, rec.emitted[-1], u[2 * om.SAMPLE_SLOTS], CDF_EPS), "final draw"
+            a_o, w_o, p_o, q_o = _decisions(st.last_draft_logits, st.last_verify_logits, orc.drafts, u, T)
+            assert a_o == orc.accepted
+            if a_g != a_o:
+                j = min(a_g, a_o)
+                d = orc.drafts[j]
+                margin = abs(u[om.SAMPLE_SLOTS + j] * q_o[j][d] - p_o[j][d])
+                assert margin <= _spread(eps, T) * (p_o[j][d] + q_o[j][d]), ("acceptance", j, margin)
+                diverged = True
+            elif rec.emitted[-1] != orc.emitted[-1]:
+                assert draw_consistent(w_o, rec.emitted[-1], u[2 * om.SAMPLE_SLOTS], _spread(eps, T)), "final"
+                diverged = True
+        if not diverged:
+            assert rec.accepted == orc.accepted and rec.emitted == orc.emitted, (rec, orc)
+            sl, pend, table = eng.lede_get_kv_state()
+            assert (sl, pend) == (orc.seq_len, st.pending)
+            assert table == orc.block_table
+            assert abs(rec.reward - orc.reward) < 1e-5
+        else:
+            rep.substitutions += 1
             eng.lede_truncate(c0)
             eng.lede_prefill([pending0] + orc.emitted[:-1])
             eng.lede_set_pending(st.pending)

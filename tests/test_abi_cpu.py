@@ -90,3 +90,18 @@ def test_read_probe_rejects_bad_arguments(lib):
     assert lib.lede_op_read_probe(src, 1024, sink, 0, None, None) == lede.LEDE_E_ARG
     assert lib.lede_op_read_probe(src, 1024, sink, 65536, None, None) == lede.LEDE_E_ARG
     assert lib.lede_op_read_probe(src, 1024, None, 4, None, None) == lede.LEDE_E_ARG
+
+
+def test_sampling_entry_points_reject_bad_arguments(lib):
+    from paper_2606_03113_amd import lede
+    tok = ctypes.c_int32()
+    x = ctypes.c_void_p(4096)
+    assert lib.lede_op_sample(None, 16, 0.6, 0.5, ctypes.byref(tok), None) == lede.LEDE_E_ARG
+    assert lib.lede_op_sample(x, 0, 0.6, 0.5, ctypes.byref(tok), None) == lede.LEDE_E_ARG
+    for t in (0.0, -1.0, float("inf"), float("nan")):
+        assert lib.lede_op_sample(x, 16, t, 0.5, ctypes.byref(tok), None) == lede.LEDE_E_ARG
+    for u in (1.0, -0.1, float("nan")):
+        assert lib.lede_op_sample(x, 16, 0.6, u, ctypes.byref(tok), None) == lede.LEDE_E_ARG
+    assert lib.lede_op_sample(x, 16, 0.6, 0.5, None, None) == lede.LEDE_E_ARG
+    u = (ctypes.c_float * lede.SAMPLE_STRIDE)()
+    assert lib.lede_step_sampled(None, None, 0, 4, 0.6, u, None, None) == lede.LEDE_E_ARG
