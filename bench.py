@@ -50,8 +50,9 @@ def verify_bytes(m, k, c):
 
 
 def kernel_source_sha():
+    """Hash of the sources the weight-streaming linear kernels are built from."""
     h = hashlib.sha256()
-    for f in ("kernels.hip", "kernels.h"):
+    for f in ("linear.hip", "device.h", "kernels.h"):
         h.update(open(os.path.join(ROOT, "paper_2606_03113_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 

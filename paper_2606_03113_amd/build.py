@@ -6,7 +6,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 SO = os.path.join(HERE, "liblede.so")
-SOURCES = ["kernels.hip", "runtime.cpp"]
+SOURCES = ["linear.hip", "norm.hip", "attention.hip", "accept.hip", "misc.hip", "runtime.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
@@ -17,10 +17,11 @@ FLAGS = [
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link the shared library (always rebuilds)."""
-    objs = []
+    """Compile every source (in parallel) and link the shared library (always
+    rebuilds)."""
     build_dir = os.path.join(HERE, "_build")
     os.makedirs(build_dir, exist_ok=True)
+    procs, objs = [], []
     for src in SOURCES:
         path = os.path.join(CSRC, src)
         obj = os.path.join(build_dir, src + ".o")
@@ -29,8 +30,11 @@ def build(verbose: bool = False) -> str:
             cmd[1:1] = ["-x", "hip"]
         if verbose:
             print(" ".join(cmd), file=sys.stderr)
-        subprocess.check_call(cmd)
+        procs.append((src, subprocess.Popen(cmd)))
         objs.append(obj)
+    failed = [src for src, p in procs if p.wait() != 0]
+    if failed:
+        raise RuntimeError("compilation failed: " + ", ".join(failed))
     tmp = SO + ".tmp%d" % os.getpid()
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, SO)

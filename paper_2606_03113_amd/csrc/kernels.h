@@ -1,5 +1,6 @@
 // Internal interface between the runtime (runtime.cpp) and the gfx950
-// kernels (kernels.hip).  Not part of the public C ABI.
+// kernels (linear.hip, norm.hip, attention.hip, accept.hip, misc.hip).  Not
+// part of the public C ABI.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stddef.h>
@@ -161,7 +162,8 @@ struct SampledAcceptArgs {
   const float* u;                // the step's uniforms
 };
 
-// Launchers (kernels.hip).  All return hipError_t of the launch.
+// Launchers (one per kernel family, next to its kernels).  All return
+// hipError_t of the launch.
 hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s);
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s);
 // e0 / e1 (optional): events recorded by the dispatch at kernel start / end.

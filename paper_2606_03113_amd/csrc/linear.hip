@@ -1,0 +1,397 @@
+// Weight-streaming linear kernels of the decode step (gfx950).
+//
+// Memory-bound batch-1 decoding: every weight byte is streamed from HBM once
+// per pass.  Weights live in the tiled layout of kernels.h (one coalesced
+// 1 KiB wave load per 16-row x TK tile).  The draft path (one row) uses the
+// vector dot2 instructions; the verify path (k+1 <= 16 rows) uses the
+// 16x16x32 bf16 (or 16x16x4 fp32) matrix-core instructions with the weight
+// tile as the A operand, so one weight read serves every verify row.
+//
+// Determinism: every reduction runs in a fixed order, and the matrix-core
+// result for a row does not depend on the other rows of the call, so a row
+// gives the same bits in a prefill chunk, a verify pass or a one-row
+// autoregressive step.
+#include "device.h"
+
+namespace lede {
+
+// ---- repack: logical row-major -> tiled -------------------------------------
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_repack(RepackArgs a) {
+  typedef Tile<DT> TL;
+  typedef typename Elem<DT>::T ET;
+  const size_t total = (size_t)a.n_groups * a.KT * 64;
+  for (size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x; idx < total; idx += (size_t)gridDim.x * 256) {
+    const int lane = (int)(idx & 63);
+    const size_t rest = idx >> 6;
+    const int t = (int)(rest % a.KT);
+    const int gl = (int)(rest / a.KT);  // group within this call
+    const int r = lane & 15;
+    int row;
+    bool valid = true;
+    switch (a.order) {
+      case ROWS_ROPE: {
+        const int gph = a.hd / 16;
+        const int head = gl / gph, tt = gl % gph;
+        row = head * a.hd + (r < 8 ? 8 * tt + r : a.hd / 2 + 8 * tt + (r - 8));
+        break;
+      }
+      case ROWS_GATE: row = 8 * gl + r; valid = r < 8; break;
+      case ROWS_UP: row = 8 * gl + (r - 8); valid = r >= 8; break;
+      default: row = 16 * gl + r;
+    }
+    if (!valid) continue;  // the other source fills these rows
+    ET vals[TL::EPL];
+    const int k0 = t * TL::TK + (lane >> 4) * TL::EPL;
+#pragma unroll
+    for (int e = 0; e < TL::EPL; ++e) {
+      const int k = k0 + e;
+      vals[e] = (row < a.N && k < a.K) ? ((const ET*)a.src)[(size_t)row * a.K + k] : (ET)0;
+    }
+    uint8_t* dst = (uint8_t*)a.dst + ((size_t)(a.group0 + gl) * a.KT + t) * TILE_BYTES + lane * 16;
+    *(uint4*)dst = *(const uint4*)vals;
+  }
+}
+
+// ---- linear: y = W x with fused prologue / epilogue --------------------------
+
+template <int DT>
+__device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best) {
+  const int tid = threadIdx.x;
+  const int M = a.M;
+  switch (a.epi) {
+    case EPI_STORE: {
+      const int n = tid >> 4, m = tid & 15;
+      if (m < M) a.out[(size_t)m * a.ldo + g * 16 + n] = ct[n][m];
+      break;
+    }
+    case EPI_BIAS_RELU: {
+      if (tid < 16) {
+        const int row = g * 16 + tid;
+        a.out[row] = fmaxf(ct[tid][0] + a.bias[row], 0.f);
+      }
+      break;
+    }
+    case EPI_RESID: {
+      const int n = tid >> 4, m = tid & 15;
+      if (m < M) a.h[(size_t)m * a.ldh + g * 16 + n] += ct[n][m];
+      break;
+    }
+    case EPI_SWIGLU: {
+      if (tid < 128) {
+        const int r = tid >> 4, m = tid & 15;
+        if (m < M) {
+          const float gt = ct[r][m], up = ct[r + 8][m];
+          const float s = gt / (1.f + __expf(-gt));
+          Elem<DT>::store(a.act, (size_t)m * a.ld_act + 8 * g + r, s * up);
+        }
+      }
+      break;
+    }
+    case EPI_QKV: {
+      const int hd = a.hd, gph = hd / 16;
+      const int qg = a.nq * gph, kg = a.nkv * gph;
+      const int c = *a.seq_len + a.pos_off;
+      if (g < qg + kg) {
+        if (tid < 128) {
+          const int r = tid >> 4, m = tid & 15;
+          if (m < M) {
+            const bool isq = g < qg;
+            const int gl = isq ? g : g - qg;
+            const int head = gl / gph, i = 8 * (gl % gph) + r;
+            const int pos = c + m;
+            const float2 cs = a.rope[(size_t)pos * (hd / 2) + i];
+            const float x0 = ct[r][m], x1 = ct[r + 8][m];
+            const float y0 = x0 * cs.x - x1 * cs.y;
+            const float y1 = x1 * cs.x + x0 * cs.y;
+            if (isq) {
+              float* q = a.q + (size_t)m * a.ldq + head * hd;
+              q[i] = y0;
+              q[i + hd / 2] = y1;
+            } else {
+              const int page = a.block_table[pos >> 6];
+              const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+              Elem<DT>::store(a.kcache, base + i, y0);
+              Elem<DT>::store(a.kcache, base + i + hd / 2, y1);
+            }
+          }
+        }
+      } else {
+        const int n = tid >> 4, m = tid & 15;
+        if (m < M) {
+          const int dim = (g - qg - kg) * 16 + n;
+          const int head = dim / hd, i = dim % hd;
+          const int pos = c + m;
+          const int page = a.block_table[pos >> 6];
+          const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+          Elem<DT>::store(a.vcache, base + i, ct[n][m]);
+        }
+      }
+      break;
+    }
+    case EPI_ARGMAX: {
+      const int n = tid >> 4, m = tid & 15;
+      const int row = g * 16 + n;
+      if (m < M && a.logits) a.logits[(size_t)m * a.ld_logits + row] = ct[n][m];
+      if (tid < 16 && tid < M) {
+        for (int nn = 0; nn < 16; ++nn) {
+          const int rr = g * 16 + nn;
+          if (rr < a.vocab) {
+            const uint64_t key = argmax_key(ct[nn][tid], rr);
+            best = key > best ? key : best;
+          }
+        }
+      }
+      break;
+    }
+  }
+}
+
+
+// Deterministic sum over the NW wavefronts of a block (every thread takes
+// part in the barriers).
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* scratch) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) scratch[wave] = v;
+  __syncthreads();
+  float s = scratch[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) s += scratch[w];
+  return s;
+}
+
+// Normalise the single input row of the vector kernel into LDS with every
+// thread of the block: thread t holds elements 4t + 4 NT j of the row and of
+// the gain in registers (both requested together), sums the squares in j
+// order, and the block sums the threads' partials in wave order.  The row is
+// zero-padded to the batch size the main loop reads.
+template <int DT, int NW>
+__device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch) {
+  constexpr int NT = NW * 64, J = (8192 + 4 * NT - 1) / (4 * NT);  // rows of up to 8192 elements
+  const int tid = threadIdx.x;
+  const int row_bytes = a.K * Elem<DT>::ES_, pad_bytes = lin_x_tiles(a.KT) * Tile<DT>::TK * Elem<DT>::ES_;
+  for (int i = row_bytes + tid * 4; i < pad_bytes; i += NT * 4) *(uint32_t*)(lds + i) = 0u;
+  const float* h = a.h;
+  const void* row = nullptr;
+  float* h_out = nullptr;
+  if (a.x_mode == X_EMBED_NORM) {
+    const int tok = (int)min((unsigned)a.tok.get(0), (unsigned)(a.vocab - 1));
+    row = (const uint8_t*)a.embed + (size_t)tok * a.K * Elem<DT>::ES_;
+    if (blockIdx.x == 0) h_out = a.h;
+    h = nullptr;
+  }
+  float4 v[J], g[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    const bool in = i < a.K;
+    v[j] = in ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    g[j] = in ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    ss = fmaf(v[j].x, v[j].x, ss);
+    ss = fmaf(v[j].y, v[j].y, ss);
+    ss = fmaf(v[j].z, v[j].z, ss);
+    ss = fmaf(v[j].w, v[j].w, ss);
+  }
+  ss = block_sum<NW>(ss, scratch);
+  const float inv = rsqrtf(ss / (float)a.K + a.eps);
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int i = 4 * tid + 4 * NT * j;
+    if (i < a.K) {
+      float4 y;
+      y.x = (v[j].x * inv) * g[j].x;
+      y.y = (v[j].y * inv) * g[j].y;
+      y.z = (v[j].z * inv) * g[j].z;
+      y.w = (v[j].w * inv) * g[j].w;
+      if (h_out) *(float4*)(h_out + i) = v[j];
+      store4<DT>(lds, i, y);
+    }
+  }
+  __syncthreads();
+}
+
+// Copy the vector kernel's input row (KT tiles of the model dtype) into LDS
+// and zero the padding up to pad bytes.
+template <int NW>
+__device__ void stage_copy_row(const void* x, int bytes, int pad, uint8_t* lds) {
+  for (int i = threadIdx.x * 16; i < pad; i += NW * 64 * 16)
+    *(uint4*)(lds + i) = i < bytes ? ld16((const uint8_t*)x + i) : make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+}
+
+// y = W x over 16-row groups, one group per block pass.  Eight wavefronts
+// split K (wave w takes tiles w, w + 8, ...), four tiles per wave in flight,
+// and the partials are summed in wave order.
+//   XS = XS_LDS:    one input row, staged in LDS in the prologue (normalised
+//                   for X_NORM / X_EMBED_NORM, copied otherwise); dot2 math.
+//   XS = XS_GLOBAL: one input row read from global memory per tile (rows too
+//                   long for LDS); dot2 math.
+//   XS = XS_MFMA:   up to 16 rows read from global memory (normalised by the
+//                   norm kernel), 16x16 matrix-core tiles.
+template <int DT, int XS>
+__global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
+  typedef Tile<DT> TL;
+  constexpr int NW = LIN_WAVES, U = 4;  // tiles per wave per batch
+  constexpr bool MFMA = XS == XS_MFMA;
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ float red[NW][16][16];
+  __shared__ float ct[16][17];
+  __shared__ float scratch[NW];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int KT = a.KT, NG = a.n_groups;
+  const uint4 zero = {0u, 0u, 0u, 0u};
+
+  if (blockIdx.x == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
+
+  int g = blockIdx.x;
+  // the weights do not depend on the input: the first batch is in flight
+  // while the prologue stages the input row
+  uint4 w[U];
+  {
+    const uint8_t* wg = a.w + (size_t)(g < NG ? g : 0) * KT * TILE_BYTES + lane * 16;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = wave + NW * u;
+      w[u] = (g < NG && t < KT) ? ld16_stream(wg + (size_t)t * TILE_BYTES) : zero;
+    }
+  }
+  if (XS == XS_LDS) {
+    if (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM) stage_norm_row<DT, NW>(a, smem, scratch);
+    else stage_copy_row<NW>(a.x, KT * TL::TK * TL::ES, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
+  }
+
+  uint64_t best = 0;
+  bool first = true;
+  for (; g < NG; g += gridDim.x, first = false) {
+    const uint8_t* wg = a.w + (size_t)g * KT * TILE_BYTES + lane * 16;
+    float acc0 = 0.f, acc1 = 0.f;
+    f32x4 c0 = {0.f, 0.f, 0.f, 0.f}, c1 = {0.f, 0.f, 0.f, 0.f};
+    const int m = MFMA ? (lane & 15) : 0;
+    const bool has = !MFMA || m < a.M;
+    const uint8_t* xg = (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
+    const uint8_t* xs = smem + (lane >> 4) * 16;
+    for (int t = wave; t < KT; t += NW * U) {
+      if (!(first && t == wave)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int tt = t + NW * u;
+          w[u] = tt < KT ? ld16_stream(wg + (size_t)tt * TILE_BYTES) : zero;
+        }
+      }
+      if (XS == XS_LDS) {
+#pragma unroll
+        for (int u = 0; u < U; u += 2) {
+          const int t0 = t + NW * u, t1 = t0 + NW;  // the staged row is zero-padded past KT
+          const uint4 x0 = *(const uint4*)(xs + (size_t)t0 * TL::TK * TL::ES);
+          const uint4 x1 = *(const uint4*)(xs + (size_t)t1 * TL::TK * TL::ES);
+          acc0 = dot16<DT>(w[u], x0, acc0);
+          acc1 = dot16<DT>(w[u + 1], x1, acc1);
+        }
+      } else {
+        uint4 x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int tt = t + NW * u;
+          x[u] = (has && tt < KT) ? ld16(xg + (size_t)tt * TL::TK * TL::ES) : zero;
+        }
+#pragma unroll
+        for (int u = 0; u < U; u += 2) {
+          if (MFMA) {
+            c0 = mfma_tile<DT>(w[u], x[u], c0);
+            c1 = mfma_tile<DT>(w[u + 1], x[u + 1], c1);
+          } else {
+            acc0 = dot16<DT>(w[u], x[u], acc0);
+            acc1 = dot16<DT>(w[u + 1], x[u + 1], acc1);
+          }
+        }
+      }
+    }
+    if (MFMA) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][4 * (lane >> 4) + i][lane & 15] = c0[i] + c1[i];
+    } else {
+      float acc = acc0 + acc1;
+      acc += __shfl_xor(acc, 16);
+      acc += __shfl_xor(acc, 32);
+      if (lane < 16) red[wave][lane][0] = acc;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      const int n = tid >> 4, mm = tid & 15;
+      if (MFMA || mm == 0) {
+        float s = red[0][n][mm];
+#pragma unroll
+        for (int q = 1; q < NW; ++q) s += red[q][n][mm];
+        ct[n][mm] = s;
+      }
+    }
+    __syncthreads();
+    if (tid < 256) epilogue<DT>(a, g, ct, best);
+    __syncthreads();
+  }
+  if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
+    atomicMax((unsigned long long*)&a.keys[tid], (unsigned long long)best);
+}
+
+// ---- launchers ----------------------------------------------------------------
+
+hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
+  const size_t total = (size_t)a.n_groups * a.KT * 64;
+  const int grid = (int)((total + 255) / 256 < 65536 ? (total + 255) / 256 : 65536);
+  if (dtype == 1) hipLaunchKernelGGL(k_repack<1>, dim3(grid), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(k_repack<0>, dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+int linear_x_source(int dtype, bool mfma, int K) {
+  if (mfma) return XS_MFMA;
+  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
+  return (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es <= LIN_LDS_X_MAX ? XS_LDS : XS_GLOBAL;
+}
+
+size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
+  (void)M;
+  if (linear_x_source(dtype, mfma, K) != XS_LDS) return 0;
+  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
+  const size_t row = (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es;
+  (void)x_mode;
+  return row;
+}
+
+// With events, the start / stop timestamps are taken by the dispatch itself
+// (the kernel's own execution, as a kernel trace measures it).
+template <int DT, int XS>
+static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
+                            hipEvent_t e1) {
+  if (e0)
+    hipExtLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), (uint32_t)lds, s, e0, e1, 0, a);
+  else
+    hipLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), lds, s, a);
+}
+
+hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s, hipEvent_t e0,
+                         hipEvent_t e1) {
+  const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
+  const int xs = linear_x_source(dtype, mfma, a.K);
+  if (dtype == 1) {
+    if (xs == XS_MFMA) launch_linear_t<1, XS_MFMA>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_LDS) launch_linear_t<1, XS_LDS>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<1, XS_GLOBAL>(a, grid, lds, s, e0, e1);
+  } else {
+    if (xs == XS_MFMA) launch_linear_t<0, XS_MFMA>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_LDS) launch_linear_t<0, XS_LDS>(a, grid, lds, s, e0, e1);
+    else launch_linear_t<0, XS_GLOBAL>(a, grid, lds, s, e0, e1);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace lede
