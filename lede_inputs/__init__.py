@@ -40,6 +40,7 @@ STREAM_PROMPT = 20
 STREAM_SCHED_L = 30
 STREAM_SCHED_K = 31
 STREAM_SAMPLE = 40
+STREAM_EXIT_QNET = 12
 LAYER_BASE = 1000
 LAYER_STRIDE = 16
 LAYER_TENSORS = {"wq": 1, "wk": 2, "wv": 3, "wo": 4, "wg": 6, "wu": 7, "wd": 8}
@@ -178,6 +179,17 @@ def qnet_weights(m: ModelConfig, seed: int = SEED_QNET) -> dict:
         "b1": np.zeros(h, dtype=np.float32),
         "w2": normal(seed, STREAM_QNET_W2, a * h, WEIGHT_STD, "f32").reshape(a, h),
         "b2": np.zeros(a, dtype=np.float32),
+    }
+
+
+def exit_qnet_weights(hidden: int = 16, seed: int = SEED_QNET, std: float = 0.5) -> dict:
+    """fp32 2-action exit Q-network of the paper's policy: W1 [H][3], b1 [H],
+    W2 [2][H], b2 [2] = 0 (rows of W2: continue, exit)."""
+    return {
+        "w1": normal(seed, STREAM_EXIT_QNET, hidden * 3, std, "f32").reshape(hidden, 3),
+        "b1": normal(seed, STREAM_EXIT_QNET + 1, hidden, std, "f32"),
+        "w2": normal(seed, STREAM_EXIT_QNET + 2, 2 * hidden, std, "f32").reshape(2, hidden),
+        "b2": np.zeros(2, dtype=np.float32),
     }
 
 

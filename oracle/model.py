@@ -24,6 +24,12 @@ Readings where the paper is silent:
   with k clamped to N - n_gen - 1;
 * the reward is summed over the drafts up to and including the first
   rejected one; continue penalties do not arise with a joint action;
+* the paper's exit policy: the confidence feature is the mean -log p of the
+  5 most likely tokens, the entropy is in nats, both at temperature 1; the
+  trace is the mean -log max p of the full model over the last 20 committed
+  tokens (the prompt's next token included; 0 before any); a 'continue' after
+  a draft pass ends drafting without keeping that pass's token; at most 12
+  drafts;
 * sampling: draws are inverse-CDF in index order from a uniform the caller
   supplies; acceptance keeps draft d while u < p(d) / q(d); the token after
   a rejection comes from the normalised max(0, p - q), after k acceptances
@@ -283,6 +289,8 @@ class StepRecord:
     draft_info: List[ArgmaxInfo] = field(default_factory=list)
     verify_info: List[ArgmaxInfo] = field(default_factory=list)
     block_table: List[int] = field(default_factory=list)
+    decisions: list = field(default_factory=list)   # exit policy: (kind, layer / draft, state, Q, action)
+    c_trace: float = 0.0
 
 
 def greedy_ar(dec: OracleDecoder, prompt: Sequence[int], n_gen: int):
@@ -350,8 +358,53 @@ def speculative_accept(p_rows: Sequence[np.ndarray], q_rows: Sequence[np.ndarray
     return a, y
 
 
+# ---- the paper's exit policy (Sections 3.1.1, 3.1.2, 3.3) -------------------
+
+POLICY_TOPK = 5        # tokens in the confidence feature
+POLICY_TRACE = 20      # window of the confidence trace
+POLICY_MAX_DRAFT = 12  # longest speculation of the adaptive drafting
+
+
+def log_probs(z: np.ndarray) -> np.ndarray:
+    """log softmax(z) in fp64."""
+    x = np.asarray(z, dtype=np.float64)
+    x = x - x.max()
+    return x - math.log(np.exp(x).sum())
+
+
+def exit_features(z: np.ndarray, c_trace: float) -> np.ndarray:
+    """State at a candidate exit layer (Section 3.1.1) from the next-token
+    logits z at that layer: the mean negative log-probability of the top-k
+    tokens, the entropy of the distribution, and the confidence trace."""
+    lp = log_probs(z)
+    top = np.sort(lp)[-POLICY_TOPK:]
+    return np.array([-top.mean(), -float(np.sum(np.exp(lp) * lp)), float(c_trace)])
+
+
+def exit_qnet(state: np.ndarray, w: dict) -> np.ndarray:
+    """Q(s, continue), Q(s, exit): W2 ReLU(W1 s + b1) + b2 in fp64 (Section 3.2)."""
+    hid = np.maximum(w["w1"].astype(np.float64) @ state + w["b1"].astype(np.float64), 0.0)
+    return w["w2"].astype(np.float64) @ hid + w["b2"].astype(np.float64)
+
+
+class ConfidenceTrace:
+    """The last POLICY_TRACE values of -log max p of the full model's
+    distribution at committed positions; C_trace is their mean, 0 while
+    empty."""
+
+    def __init__(self):
+        self.vals: deque = deque(maxlen=POLICY_TRACE)
+
+    def push_logits(self, z: np.ndarray):
+        self.vals.append(-float(log_probs(z).max()))
+
+    def value(self) -> float:
+        return float(np.mean(self.vals)) if self.vals else 0.0
+
+
 class SSDState:
-    """(c, pending token, n_gen) plus the pager and the committed output."""
+    """(c, pending token, n_gen) plus the pager, the committed output and the
+    confidence trace of the exit policy."""
 
     def __init__(self, dec: OracleDecoder, n_pages: int, page_size: int, order=None):
         self.dec = dec
@@ -361,14 +414,17 @@ class SSDState:
         self.out: List[int] = []
         self.last_draft_logits: List[np.ndarray] = []
         self.last_verify_logits: Optional[np.ndarray] = None
+        self.trace = ConfidenceTrace()
 
     def prefill(self, prompt: Sequence[int]) -> ArgmaxInfo:
         self.pager.ensure(len(prompt))
         h = self.dec.forward(prompt, 0, self.dec.m.n_layers)
-        info = argmax_info(self.dec.head(h[-1:])[0])
+        z = self.dec.head(h[-1:])[0]
+        info = argmax_info(z)
         self.c = len(prompt)
         self.pending = info.token
         self.out = [info.token]
+        self.trace.push_logits(z)
         return info
 
     def step(self, l: int, k: int, n_total: int, qnet: bool = False, use_qnet_action: bool = False) -> StepRecord:
@@ -411,6 +467,8 @@ class SSDState:
         self.pending = verify[a]
         self.out.extend(emitted)
         self.pager.truncate(self.c)
+        for j in range(a + 1):
+            self.trace.push_logits(z[j])
         return StepRecord(l=l, k_req=k, k_eff=k_eff, accepted=a, emitted=emitted, drafts=drafts,
                           verify=verify, reward=reward(a, k_eff, l, L), seq_len=self.c,
                           q_action=q_action, q_values=q_values, draft_info=dinfo, verify_info=vinfo,
@@ -452,10 +510,77 @@ class SSDState:
         self.pending = y
         self.out.extend(emitted)
         self.pager.truncate(self.c)
+        for j in range(a + 1):
+            self.trace.push_logits(z[j])
         self.last_p_rows, self.last_q_rows = p_rows, q_rows
         return StepRecord(l=l, k_req=k, k_eff=k_eff, accepted=a, emitted=emitted, drafts=drafts,
                           verify=[argmax_lowest(z[j]) for j in range(k_eff + 1)],
                           reward=reward(a, k_eff, l, L), seq_len=self.c, block_table=list(self.pager.table))
+
+
+    def step_paper(self, n_total: int, policy: dict, k_cap: int = POLICY_MAX_DRAFT) -> StepRecord:
+        """One greedy step under the paper's exit policy (Section 3.3).
+
+        Exit layer: the pending token goes up the candidate exit layers in
+        order; at each, the state (exit_features of that layer's next-token
+        logits, with the trace of committed confidences) is scored by the
+        2-action Q-network, and the first 'exit' (forced at the last
+        candidate) fixes l*.  Draft 1 is the argmax there.  Draft length:
+        each further draft pass at l* is scored the same way; 'exit' keeps its
+        argmax as the next draft, 'continue' ends drafting (that token is not
+        kept), and at most k_cap drafts are made.  Then verify, greedy
+        acceptance and commit as in step().  ``decisions`` lists
+        (kind, layer or draft index, state, Q-values, action)."""
+        dec, m = self.dec, self.dec.m
+        L = m.n_layers
+        cands = sorted(m.exits)
+        n_gen = len(self.out)
+        k_lim = max(0, min(k_cap, n_total - n_gen - 1))
+        ct = self.trace.value()
+        decisions = []
+        drafts, dz = [], []
+        l_star = cands[-1]
+        if k_lim > 0:
+            for ci, l in enumerate(cands):
+                z = dec.head(dec.forward([self.pending], self.c, l))[0]
+                st = exit_features(z, ct)
+                q = exit_qnet(st, policy)
+                act = argmax_lowest(q)
+                decisions.append(("layer", l, st, q, act))
+                if act == 1 or ci == len(cands) - 1:
+                    l_star = l
+                    break
+            drafts.append(argmax_lowest(z))
+            dz.append(z)
+            while len(drafts) < k_lim:
+                z = dec.head(dec.forward([drafts[-1]], self.c + len(drafts), l_star))[0]
+                st = exit_features(z, ct)
+                q = exit_qnet(st, policy)
+                act = argmax_lowest(q)
+                decisions.append(("draft", len(drafts) + 1, st, q, act))
+                if act != 1:
+                    break
+                drafts.append(argmax_lowest(z))
+                dz.append(z)
+        k_eff = len(drafts)
+        self.pager.ensure(self.c + k_eff + 1)
+        h = dec.forward([self.pending] + drafts, self.c, L)
+        zv = dec.head(h)
+        self.last_draft_logits = dz
+        self.last_verify_logits = zv
+        vinfo = [argmax_info(zv[i]) for i in range(k_eff + 1)]
+        verify = [v.token for v in vinfo]
+        a = accept_length(drafts, verify)
+        emitted = drafts[:a] + [verify[a]]
+        self.c += a + 1
+        self.pending = verify[a]
+        self.out.extend(emitted)
+        self.pager.truncate(self.c)
+        for j in range(a + 1):
+            self.trace.push_logits(zv[j])
+        return StepRecord(l=l_star, k_req=k_cap, k_eff=k_eff, accepted=a, emitted=emitted, drafts=drafts,
+                          verify=verify, reward=reward(a, k_eff, l_star, L), seq_len=self.c,
+                          verify_info=vinfo, block_table=list(self.pager.table), decisions=decisions, c_trace=ct)
 
 
 def ssd_generate(dec: OracleDecoder, prompt: Sequence[int], n_total: int, actions, n_pages: int,
