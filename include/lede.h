@@ -70,18 +70,25 @@ typedef struct {
   int32_t exits[64];           /* candidate exit layers, ascending, 1..n_layers */
   int32_t lengths[16];         /* candidate draft lengths, 1..16 */
   int32_t k_max;               /* largest draft length any call may use (<= 15) */
+  int32_t exit_qnet_hidden;    /* hidden width of the exit policy's 2-action Q-network
+                                  (0: no exit policy; <= 1024); its candidate layers
+                                  are exits[0 .. n_exits) */
 } lede_config;
 
 /* Tensor kinds for lede_load_tensor.  Logical layouts (row-major [out][in]):
  * EMBED, HEAD [vocab][d]; FINAL_NORM, ATTN_NORM, FFN_NORM [d];
  * WQ [n_heads*hd][d]; WK, WV [n_kv*hd][d]; WO [d][n_heads*hd];
  * WG, WU [ffn][d]; WD [d][ffn]; all in the model dtype.
- * QNET_W1 [H][d], QNET_B1 [H], QNET_W2 [E*K][H], QNET_B2 [E*K]: fp32. */
+ * QNET_W1 [H][d], QNET_B1 [H], QNET_W2 [E*K][H], QNET_B2 [E*K]: fp32.
+ * EXIT_W1 [He][3], EXIT_B1 [He], EXIT_W2 [2][He], EXIT_B2 [2]: fp32, the
+ * exit policy's Q-network (state: top-5 confidence, entropy, confidence
+ * trace; outputs: continue, exit). */
 typedef enum {
   LEDE_T_EMBED = 0, LEDE_T_FINAL_NORM, LEDE_T_HEAD,
   LEDE_T_ATTN_NORM, LEDE_T_WQ, LEDE_T_WK, LEDE_T_WV, LEDE_T_WO,
   LEDE_T_FFN_NORM, LEDE_T_WG, LEDE_T_WU, LEDE_T_WD,
-  LEDE_T_QNET_W1, LEDE_T_QNET_B1, LEDE_T_QNET_W2, LEDE_T_QNET_B2
+  LEDE_T_QNET_W1, LEDE_T_QNET_B1, LEDE_T_QNET_W2, LEDE_T_QNET_B2,
+  LEDE_T_EXIT_W1, LEDE_T_EXIT_B1, LEDE_T_EXIT_W2, LEDE_T_EXIT_B2
 } lede_tensor;
 
 /* An action of the agent: exit layer l* (1..L) and draft length k. */
@@ -202,6 +209,30 @@ int lede_step(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_
 int lede_step_sampled(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
                       float temperature, const float* uniforms, void* stream, lede_step_record* rec);
 
+/* ---- the paper's exit policy (Sections 3.1.1, 3.1.2, 3.3) -----------------
+ * Needs exit_qnet_hidden > 0.  One greedy step: the pending token goes up
+ * the candidate exit layers exits[0..n_exits) in order; at each, the state
+ * (C_5 = mean -log p of the 5 most likely tokens, H = entropy in nats, both
+ * of softmax(z) of that layer's shared final norm + LM head, and C_trace)
+ * is scored by the exit Q-network, and the first 'exit' (forced at the last
+ * candidate) fixes l*; draft 1 is that head's argmax.  Each further draft
+ * pass at l* is scored the same way: 'exit' keeps its argmax as the next
+ * draft, 'continue' ends drafting (its token is not kept); at most
+ * min(12, k_max, n_remaining - 1) drafts.  Then verify, greedy acceptance,
+ * truncation.  The host reads each decision back (one synchronisation per
+ * decision).  rec->k_req = 12, rec->l = l*.  The decisions are read with
+ * lede_debug_read(which = 4).
+ *
+ * C_trace is the mean of -log max p of the full model at the last 20
+ * committed positions (0 while none): every prefill (its last row) and every
+ * verify (the accepted rows and the bonus row) of a context with an exit
+ * policy push to the window, whichever call made them.  lede_truncate does
+ * not rewind it; lede_set_trace replaces it (host values, oldest first,
+ * n <= 20), lede_get_trace reads it (n receives the count). */
+int lede_step_policy(lede_ctx* ctx, int32_t n_remaining, void* stream, lede_step_record* rec);
+int lede_set_trace(lede_ctx* ctx, const float* values, int32_t n, void* stream);
+int lede_get_trace(lede_ctx* ctx, float* values /* [20] */, int32_t* n, void* stream);
+
 /* Committed KV length, pending token and the page table (host copies). */
 int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t* block_table,
                       int32_t cap, int32_t* n_table);
@@ -209,8 +240,11 @@ int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t
 /* Debug read-back (needs set_options(debug=1)); which = 0: logits of the
  * last verify / prefill head launch [rows][vocab] fp32; 1: Q-values of the
  * last Q-network run [E*K]; 2: the Q-network's input state [d] fp32; 3:
- * logits of the last step's draft heads [rows][vocab].  *rows receives the
- * row count.  Synchronises. */
+ * logits of the last step's draft heads [rows][vocab]; 4 (debug mode not
+ * needed): the exit-policy decisions of the last lede_step_policy, 8 floats
+ * each (kind 0 = candidate layer / 1 = draft pass, layer or draft index,
+ * C_5, H, C_trace, Q(continue), Q(exit), action).  *rows receives the row
+ * count.  Synchronises. */
 int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows,
                     void* stream);
 

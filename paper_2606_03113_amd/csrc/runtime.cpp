@@ -33,10 +33,11 @@ struct Layout {
   // weight arena offsets
   struct LayerOff { size_t attn_norm, wqkv, wo, ffn_norm, wgu, wd; };
   std::vector<LayerOff> lay;
-  size_t embed, final_norm, head, qw1, qb1, qw2, qb2, wbytes;
+  size_t embed, final_norm, head, qw1, qb1, qw2, qb2, ew1, eb1, ew2, eb2, wbytes;
+  int He;  // exit-policy Q-network hidden width (0: none)
   // workspace offsets
   size_t h, xn, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
-      record, rope, unif, dstats, wsbytes;
+      record, rope, unif, dstats, trace, trace_state, pol_out, wsbytes;
   size_t kvbytes, kv_half;
 };
 
@@ -55,7 +56,8 @@ const char* check_config(const lede_config* c) {
   if (c->max_ctx < 1 || c->n_pages < 1) return "bad KV geometry";
   if (c->k_max < 0 || c->k_max > 15) return "k_max must be in 0..15";
   if (c->qnet_hidden < 0 || c->qnet_hidden % 16) return "qnet_hidden must be a multiple of 16";
-  if (c->qnet_hidden > 0) {
+  if (c->exit_qnet_hidden < 0 || c->exit_qnet_hidden > 1024) return "exit_qnet_hidden must be in 0..1024";
+  if (c->qnet_hidden > 0 || c->exit_qnet_hidden > 0) {
     if (c->n_exits < 1 || c->n_exits > 64 || c->n_lengths < 1 || c->n_lengths > 16) return "bad action grid";
     for (int i = 0; i < c->n_exits; ++i)
       if (c->exits[i] < 1 || c->exits[i] > c->n_layers || (i && c->exits[i] <= c->exits[i - 1]))
@@ -97,6 +99,11 @@ Layout make_layout(const lede_config* c) {
   o.qb1 = take((size_t)o.H * 4);
   o.qw2 = take((size_t)o.A * o.H * 4);
   o.qb2 = take((size_t)o.A * 4);
+  o.He = c->exit_qnet_hidden;
+  o.ew1 = take((size_t)o.He * 3 * 4);
+  o.eb1 = take((size_t)o.He * 4);
+  o.ew2 = take((size_t)o.He * 2 * 4);
+  o.eb2 = take(o.He ? 2 * 4 : 0);
   o.wbytes = off;
 
   off = 0;
@@ -120,6 +127,9 @@ Layout make_layout(const lede_config* c) {
   o.rope = take((size_t)o.max_ctx * (o.hd / 2) * 8);
   o.unif = take(UNIF_FLOATS * 4);
   o.dstats = take(2 * SAMPLE_SLOTS * 4);
+  o.trace = take(POLICY_TRACE * 4);
+  o.trace_state = take(4 * 4);
+  o.pol_out = take(POLICY_LOG * 4);
   o.wsbytes = off;
 
   o.kv_half = align256((size_t)o.L * o.n_pages * o.nkv * PAGE * o.hd * o.es);
@@ -144,6 +154,8 @@ struct lede_ctx {
   int32_t* table_h = nullptr;   // pinned mirror uploaded to the device table
   int32_t* record_h = nullptr;  // pinned read-back of the step record
   float* unif_h = nullptr;      // pinned staging of a sampled step's uniforms
+  float* trace_h = nullptr;     // pinned staging of the confidence trace and policy decisions
+  std::vector<float> policy_log;  // decisions of the last exit-policy step, POLICY_LOG floats each
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
@@ -381,14 +393,15 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       qa.embed = c->W<void>(o.embed);
       qa.tok = tok;
       qa.vocab = o.V;
-      if (first && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = vec ? 1 : M; }
+      // the pass's argmax slots are cleared by its first kernel
+      if (j == l_begin && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = vec ? 1 : M; }
     } else {
       NormArgs na{};
       na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
       na.h = c->S<float>(o.h); na.gain = c->W<void>(lw.attn_norm); na.eps = c->cfg.rms_eps;
       na.embed = first; na.embed_w = c->W<void>(o.embed); na.tok = tok; na.vocab = o.V;
       na.x = c->S<void>(o.xn);
-      if (first && zero_slot) { na.zero_keys = zero_slot; na.n_zero_keys = M; }
+      if (j == l_begin && zero_slot) { na.zero_keys = zero_slot; na.n_zero_keys = M; }
       LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
       qa.x_mode = X_PLAIN; qa.x = c->S<void>(o.xn); qa.ldx = o.d;
     }
@@ -524,14 +537,26 @@ int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_b
   return LEDE_OK;
 }
 
+// Confidence trace of the exit policy: push -log max p of `rows` logits rows
+// (or of record[0] + 1 rows when record is set).
+int push_trace(lede_ctx* c, const float* logits, int rows, const int32_t* record, hipStream_t s) {
+  TracePushArgs ta{};
+  ta.logits = logits; ta.vocab = c->lo.V; ta.ld = c->lo.V;
+  ta.record = record; ta.n_rows = rows;
+  ta.trace = c->S<float>(c->lo.trace); ta.trace_state = c->S<int32_t>(c->lo.trace_state);
+  LAUNCH(LEDE_K_ACCEPT, (double)(rows ? rows : 2) * c->lo.V * 4, launch_trace_push(ta, s));
+  return LEDE_OK;
+}
+
 int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f) {
   uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
   uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
   const bool sampled = inv_t > 0.f;
+  const bool trace = c->lo.He > 0;
   TokenSrc tok{nullptr, dk};
   int rc = run_layers(c, k + 1, false, tok, 0, 0, c->lo.L, 0, vk, s);
   if (rc) return rc;
-  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled), s);
+  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s);
   if (rc) return rc;
   AcceptArgs aa{};
   aa.dkeys = dk; aa.vkeys = vk; aa.k = k;
@@ -550,6 +575,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f) {
   } else {
     LAUNCH(LEDE_K_ACCEPT, 256.0, launch_accept(aa, s));
   }
+  if (trace && (rc = push_trace(c, verify_logits(c, true), 0, aa.record, s))) return rc;
   c->last_rows = k + 1;
   return LEDE_OK;
 }
@@ -633,6 +659,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
   if (hipHostMalloc((void**)&c->table_h, (size_t)o.max_pages_seq * 4 + 256, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->record_h, RECORD_INTS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->unif_h, UNIF_FLOATS * 4, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->trace_h, 64 * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->keys_h, 32 * 8, 0) != hipSuccess) {
     lede_destroy(c);
     return LEDE_E_HIP;
@@ -667,6 +694,7 @@ void lede_destroy(lede_ctx* c) {
   if (c->table_h) (void)hipHostFree(c->table_h);
   if (c->record_h) (void)hipHostFree(c->record_h);
   if (c->unif_h) (void)hipHostFree(c->unif_h);
+  if (c->trace_h) (void)hipHostFree(c->trace_h);
   if (c->keys_h) (void)hipHostFree(c->keys_h);
   delete c;
 }
@@ -709,6 +737,10 @@ int lede_load_tensor(lede_ctx* c, int32_t kind, int32_t layer, const void* src, 
     case LEDE_T_QNET_B1: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qb1, (size_t)o.H * 4);
     case LEDE_T_QNET_W2: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qw2, (size_t)o.A * o.H * 4);
     case LEDE_T_QNET_B2: if (!o.H) return fail(c, LEDE_E_STATE, "config has no Q-network"); return copy(o.qb2, (size_t)o.A * 4);
+    case LEDE_T_EXIT_W1: if (!o.He) return fail(c, LEDE_E_STATE, "config has no exit policy"); return copy(o.ew1, (size_t)o.He * 3 * 4);
+    case LEDE_T_EXIT_B1: if (!o.He) return fail(c, LEDE_E_STATE, "config has no exit policy"); return copy(o.eb1, (size_t)o.He * 4);
+    case LEDE_T_EXIT_W2: if (!o.He) return fail(c, LEDE_E_STATE, "config has no exit policy"); return copy(o.ew2, (size_t)o.He * 2 * 4);
+    case LEDE_T_EXIT_B2: if (!o.He) return fail(c, LEDE_E_STATE, "config has no exit policy"); return copy(o.eb2, 2 * 4);
   }
   return fail(c, LEDE_E_ARG, "unknown tensor kind %d", kind);
 }
@@ -755,7 +787,11 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
     const int M = std::min(MROWS, n - off);
     TokenSrc tok{pd + off, nullptr};
     rc = run_layers(c, M, false, tok, off, 0, c->lo.L, 0, vk, s);
-    if (!rc && off + M == n) rc = run_head(c, M, false, vk, verify_logits(c), s);
+    if (!rc && off + M == n) {
+      const bool trace = c->lo.He > 0;
+      rc = run_head(c, M, false, vk, verify_logits(c, trace), s);
+      if (!rc && trace) rc = push_trace(c, verify_logits(c, true) + (size_t)(M - 1) * c->lo.V, 1, nullptr, s);
+    }
     if (rc) { truncate_pages(c, c0); (void)saved_table; return rc; }
     last_m = M;
   }
@@ -989,6 +1025,119 @@ int lede_step_sampled(lede_ctx* c, const lede_action* forced, int32_t log_qnet, 
   return step_impl(c, forced, log_qnet, n_remaining, temperature, uniforms, stream, rec);
 }
 
+int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_record* rec) {
+  if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  const Layout& o = c->lo;
+  if (!o.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
+  hipStream_t s = S_(stream);
+  memset(rec, 0, sizeof *rec);
+  rec->q_action = -1;
+  rec->q_max = NAN;
+  c->policy_log.clear();
+  const int c0 = c->seq_len;
+  const int k_lim = std::max(0, std::min(std::min(POLICY_MAX_DRAFT, o.k_max), n_remaining - 1));
+  int rc;
+  if ((rc = ensure_pages(c, c0 + k_lim + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+  uint64_t* dk = c->S<uint64_t>(o.dkeys);
+  ExitPolicyArgs pa{};
+  pa.vocab = o.V; pa.hidden = o.He;
+  pa.w1 = c->W<float>(o.ew1); pa.b1 = c->W<float>(o.eb1); pa.w2 = c->W<float>(o.ew2); pa.b2 = c->W<float>(o.eb2);
+  pa.trace = c->S<float>(o.trace); pa.trace_state = c->S<int32_t>(o.trace_state);
+  pa.out = c->S<float>(o.pol_out);
+  // one decision: the state of the head's logits, scored on the device, read back
+  auto decide = [&](const float* logits, int kind, int index, int* action) -> int {
+    pa.logits = logits; pa.kind = (float)kind; pa.index = (float)index;
+    HIP_CHECK(c, launch_exit_policy(pa, s));
+    HIP_CHECK(c, hipMemcpyAsync(c->trace_h, pa.out, POLICY_LOG * 4, hipMemcpyDeviceToHost, s));
+    HIP_CHECK(c, hipStreamSynchronize(s));
+    c->policy_log.insert(c->policy_log.end(), c->trace_h, c->trace_h + POLICY_LOG);
+    *action = c->trace_h[7] > 0.5f ? 1 : 0;
+    return LEDE_OK;
+  };
+  int l_star = c->cfg.exits[c->cfg.n_exits - 1], k = 0;
+  if (k_lim > 0) {
+    // exit layer: up the candidate layers with the pending token (draft pass 1)
+    int begin = 0;
+    for (int e = 0; e < c->cfg.n_exits; ++e) {
+      const int l = c->cfg.exits[e];
+      rc = run_layers(c, 1, true, TokenSrc{nullptr, dk}, 0, begin, l, 0, dk + 1, s);
+      if (!rc) rc = run_head(c, 1, true, dk + 1, draft_logits(c, 0, true), s);
+      int act = 0;
+      if (!rc) rc = decide(draft_logits(c, 0, true), 0, l, &act);
+      if (rc) { truncate_pages(c, c0); return rc; }
+      begin = l;
+      if (act == 1 || e == c->cfg.n_exits - 1) {
+        l_star = l;
+        break;
+      }
+    }
+    k = 1;
+    // draft length: each further pass at l* continues on 'exit'
+    while (k < k_lim) {
+      rc = run_layers(c, 1, true, TokenSrc{nullptr, dk + k}, k, 0, l_star, 0, dk + k + 1, s);
+      if (!rc) rc = run_head(c, 1, true, dk + k + 1, draft_logits(c, k, true), s);
+      int act = 0;
+      if (!rc) rc = decide(draft_logits(c, k, true), 1, k + 1, &act);
+      if (rc) { truncate_pages(c, c0); return rc; }
+      if (act != 1) break;
+      ++k;
+    }
+    c->last_draft_rows = k;
+  }
+  if ((rc = launch_verify(c, k, s))) return rc;
+  if ((rc = read_record(c, s))) return rc;
+  commit_host(c);
+  if ((rc = prof_fold(c))) return rc;
+  const int a = c->record_h[0];
+  rec->l = l_star;
+  rec->k_req = POLICY_MAX_DRAFT;
+  rec->k_eff = k;
+  rec->accepted = a;
+  rec->n_emitted = a + 1;
+  for (int i = 0; i <= a; ++i) rec->tokens[i] = c->record_h[4 + i];
+  for (int i = 0; i < k; ++i) rec->drafts[i] = c->record_h[24 + i];
+  rec->seq_len = c->record_h[2];
+  rec->pending = c->record_h[3];
+  if (k > 0) {
+    const double lam = (double)(o.L - l_star) / o.L;
+    rec->reward = (float)(a * (1.0 + lam) + (a < k ? (-2.0 + lam) : 0.0));
+  }
+  return LEDE_OK;
+}
+
+int lede_set_trace(lede_ctx* c, const float* values, int32_t n, void* stream) {
+  if (!c || (n > 0 && !values)) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->lo.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
+  if (n < 0 || n > POLICY_TRACE) return fail(c, LEDE_E_ARG, "trace length %d not in 0..%d", n, POLICY_TRACE);
+  hipStream_t s = S_(stream);
+  for (int i = 0; i < POLICY_TRACE; ++i) c->trace_h[i] = i < n ? values[i] : 0.f;
+  int32_t* st = (int32_t*)(c->trace_h + 32);
+  st[0] = n;
+  st[1] = n % POLICY_TRACE;
+  HIP_CHECK(c, hipMemcpyAsync(c->S<float>(c->lo.trace), c->trace_h, POLICY_TRACE * 4, hipMemcpyHostToDevice, s));
+  HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.trace_state), st, 2 * 4, hipMemcpyHostToDevice, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  return LEDE_OK;
+}
+
+int lede_get_trace(lede_ctx* c, float* values, int32_t* n, void* stream) {
+  if (!c || !values || !n) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->lo.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
+  hipStream_t s = S_(stream);
+  HIP_CHECK(c, hipMemcpyAsync(c->trace_h, c->S<float>(c->lo.trace), POLICY_TRACE * 4, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipMemcpyAsync(c->trace_h + 32, c->S<int32_t>(c->lo.trace_state), 2 * 4, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  const int32_t* st = (const int32_t*)(c->trace_h + 32);
+  const int cnt = st[0], next = st[1];
+  // oldest first: the ring holds the last cnt values ending just before `next`
+  for (int i = 0; i < cnt; ++i) values[i] = c->trace_h[(next - cnt + i + 2 * POLICY_TRACE) % POLICY_TRACE];
+  *n = cnt;
+  return LEDE_OK;
+}
+
 int lede_op_sample(const float* logits, int32_t V, float temperature, float u, int32_t* token, void* stream) {
   if (!logits || !token || V < 1) return LEDE_E_ARG;
   if (!(temperature > 0.f) || !std::isfinite(temperature) || !(u >= 0.f && u < 1.f)) return LEDE_E_ARG;
@@ -1022,7 +1171,7 @@ int lede_get_kv_state(lede_ctx* c, int32_t* seq_len, int32_t* pending, int32_t* 
 
 int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t* rows, void* stream) {
   if (!c || !host) return fail(c, LEDE_E_ARG, "null argument");
-  if (!c->debug) return fail(c, LEDE_E_STATE, "debug mode is off");
+  if (!c->debug && which != 4) return fail(c, LEDE_E_STATE, "debug mode is off");
   hipStream_t s = S_(stream);
   const Layout& o = c->lo;
   const float* src;
@@ -1033,6 +1182,13 @@ int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t
     case 1: r = 1; src = c->S<float>(o.qv); n = (size_t)o.A; break;
     case 2: r = 1; src = c->S<float>(o.qs); n = (size_t)o.d; break;
     case 3: r = c->last_draft_rows; src = c->S<float>(o.logits) + (size_t)MROWS * o.V; n = (size_t)r * o.V; break;
+    case 4: {
+      const size_t m = c->policy_log.size();
+      if (cap < m) return fail(c, LEDE_E_ARG, "capacity %zu < %zu", cap, m);
+      std::copy(c->policy_log.begin(), c->policy_log.end(), host);
+      if (rows) *rows = (int)(m / POLICY_LOG);
+      return LEDE_OK;
+    }
     default: return fail(c, LEDE_E_ARG, "unknown debug buffer %d", which);
   }
   if (cap < n) return fail(c, LEDE_E_ARG, "capacity %zu < %zu", cap, n);

@@ -23,7 +23,7 @@ STATUS = {0: "OK", -1: "E_ARG", -2: "E_STATE", -3: "E_KV_FULL", -4: "E_CTX_OVERF
           -6: "E_UNSUPPORTED"}
 
 T_EMBED, T_FINAL_NORM, T_HEAD, T_ATTN_NORM, T_WQ, T_WK, T_WV, T_WO, T_FFN_NORM, T_WG, T_WU, T_WD, \
-    T_QNET_W1, T_QNET_B1, T_QNET_W2, T_QNET_B2 = range(16)
+    T_QNET_W1, T_QNET_B1, T_QNET_W2, T_QNET_B2, T_EXIT_W1, T_EXIT_B1, T_EXIT_W2, T_EXIT_B2 = range(20)
 LAYER_KINDS = {"attn_norm": T_ATTN_NORM, "wq": T_WQ, "wk": T_WK, "wv": T_WV, "wo": T_WO,
                "ffn_norm": T_FFN_NORM, "wg": T_WG, "wu": T_WU, "wd": T_WD}
 
@@ -35,7 +35,7 @@ class LedeConfig(ctypes.Structure):
                 ("dtype", ctypes.c_int32), ("max_ctx", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("n_pages", ctypes.c_int32), ("qnet_hidden", ctypes.c_int32), ("n_exits", ctypes.c_int32),
                 ("n_lengths", ctypes.c_int32), ("exits", ctypes.c_int32 * 64), ("lengths", ctypes.c_int32 * 16),
-                ("k_max", ctypes.c_int32)]
+                ("k_max", ctypes.c_int32), ("exit_qnet_hidden", ctypes.c_int32)]
 
 
 class LedeProfEntry(ctypes.Structure):
@@ -65,7 +65,8 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
             "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
-            "lede_op_read_probe", "lede_step_sampled", "lede_op_sample"]
+            "lede_op_read_probe", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
+            "lede_get_trace"]
 SAMPLE_SLOTS = 16
 SAMPLE_STRIDE = 33
 
@@ -109,6 +110,9 @@ def load(path: str = LIB_PATH):
     L.lede_step_sampled.argtypes = [vp, P(LedeAction), i32, i32, ctypes.c_float, P(ctypes.c_float), vp,
                                     P(LedeStepRecord)]
     L.lede_op_sample.argtypes = [vp, i32, ctypes.c_float, ctypes.c_float, P(i32), vp]
+    L.lede_step_policy.argtypes = [vp, i32, vp, P(LedeStepRecord)]
+    L.lede_set_trace.argtypes = [vp, P(ctypes.c_float), i32, vp]
+    L.lede_get_trace.argtypes = [vp, P(ctypes.c_float), P(i32), vp]
     for name in EXPORTED:
         if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes"):
             getattr(L, name).restype = ctypes.c_int
@@ -122,8 +126,11 @@ class LedeError(RuntimeError):
         self.code = code
 
 
-def make_config(model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15) -> LedeConfig:
-    """lede_config from a model shape (any object with the ModelConfig fields)."""
+def make_config(model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15,
+                exit_hidden: int = 0) -> LedeConfig:
+    """lede_config from a model shape (any object with the ModelConfig fields);
+    exit_hidden > 0 adds the paper's exit policy (its candidate layers are the
+    model's exits)."""
     c = LedeConfig()
     c.n_layers, c.d_model, c.n_heads = model.n_layers, model.d_model, model.n_heads
     c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab = model.n_kv_heads, model.head_dim, model.ffn_dim, model.vocab
@@ -138,6 +145,7 @@ def make_config(model, max_ctx: int, n_pages: Optional[int] = None, k_max: int =
     for i, k in enumerate(model.lengths):
         c.lengths[i] = k
     c.k_max = k_max
+    c.exit_qnet_hidden = exit_hidden
     return c
 
 
@@ -163,12 +171,13 @@ class StepRecord:
 class Engine:
     """A liblede context over torch-allocated device regions."""
 
-    def __init__(self, model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15, device: int = 0):
+    def __init__(self, model, max_ctx: int, n_pages: Optional[int] = None, k_max: int = 15, device: int = 0,
+                 exit_hidden: int = 0):
         import torch
         self.torch = torch
         self.L = load()
         self.model = model
-        self.cfg = make_config(model, max_ctx, n_pages, k_max)
+        self.cfg = make_config(model, max_ctx, n_pages, k_max, exit_hidden)
         wb, kvb, wsb = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
         self._check(self.L.lede_region_bytes(ctypes.byref(self.cfg), ctypes.byref(wb), ctypes.byref(kvb),
                                              ctypes.byref(wsb)), None)
@@ -288,6 +297,34 @@ class Engine:
                                              u.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), self.stream,
                                              ctypes.byref(rec)), self.ctx)
         return self._record(rec)
+
+    def load_exit_qnet(self, w: dict):
+        """The exit policy's Q-network: lede_inputs.exit_qnet_weights() layout."""
+        for kind, name in ((T_EXIT_W1, "w1"), (T_EXIT_B1, "b1"), (T_EXIT_W2, "w2"), (T_EXIT_B2, "b2")):
+            self.load_tensor(kind, 0, np.ascontiguousarray(w[name], dtype=np.float32))
+
+    def lede_step_policy(self, n_remaining: int = 1 << 30) -> StepRecord:
+        rec = LedeStepRecord()
+        self._check(self.L.lede_step_policy(self.ctx, int(n_remaining), self.stream, ctypes.byref(rec)), self.ctx)
+        return self._record(rec)
+
+    def policy_log(self) -> np.ndarray:
+        """Decisions of the last lede_step_policy: rows of (kind, layer / draft,
+        C_5, H, C_trace, Q(continue), Q(exit), action)."""
+        out, rows = self.lede_debug_read(4, 64 * 8)
+        return out[:rows * 8].reshape(rows, 8)
+
+    def lede_set_trace(self, values):
+        v = np.ascontiguousarray(values, dtype=np.float32)
+        self._check(self.L.lede_set_trace(self.ctx, v.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), len(v),
+                                          self.stream), self.ctx)
+
+    def lede_get_trace(self) -> np.ndarray:
+        v = np.zeros(20, dtype=np.float32)
+        n = ctypes.c_int32()
+        self._check(self.L.lede_get_trace(self.ctx, v.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                          ctypes.byref(n), self.stream), self.ctx)
+        return v[:n.value]
 
     def lede_get_kv_state(self):
         """(seq_len, pending, block table)."""

@@ -265,3 +265,90 @@ def check_sampled(eng, st: SSDState, model, n_total, actions, T, rep: Report, st
             assert (sl, pend) == (st.c, st.pending)
             assert table == orc.block_table
     return rep
+
+
+# ---- the paper's exit policy ------------------------------------------------------
+
+def _qnet_lipschitz(w):
+    """|dQ| <= lip * max |ds| for the policy MLP (ReLU is 1-Lipschitz)."""
+    l1 = np.abs(w["w1"].astype(np.float64)).sum(axis=1)
+    return float(np.max(np.abs(w["w2"].astype(np.float64)) @ l1))
+
+
+def check_policy(eng, st: SSDState, model, n_total, policy, rep: Report, logit_eps=None):
+    """Greedy steps under the paper's exit policy on the GPU against the
+    oracle's step_paper: decision by decision the kind and index must match,
+    the state within the feature tolerance and the Q-values within what the
+    network turns it into; an action may differ only where the oracle's
+    Q-margin is within that tolerance (a near tie: the GPU is resynchronised
+    onto the oracle's committed state and trace).  Without a near tie the
+    drafts, acceptance, tokens, KV state and trace must match."""
+    dt = model.dtype
+    lip = _qnet_lipschitz(policy)
+    i = 0
+    while len(st.out) < n_total:
+        i += 1
+        c0, pending0 = st.c, st.pending
+        n_rem = n_total - len(st.out)
+        orc = st.step_paper(n_total, policy)
+        rec = eng.lede_step_policy(n_remaining=n_rem)
+        log = eng.policy_log()
+        rep.steps += 1
+        diverged = False
+        for j, d in enumerate(orc.decisions):
+            kind, idx, s_o, q_o, a_o = d
+            if kind == "draft":
+                # its input tokens are drafts 1 .. idx-1: a near tie in one of
+                # them changes every later state
+                for t in range(idx - 1):
+                    if rec.drafts[t] != orc.drafts[t]:
+                        rep.token(dt, rec.drafts[t], st.last_draft_logits[t])
+                        diverged = True
+                        break
+                if diverged:
+                    break
+            assert j < len(log), ("GPU made fewer decisions", j, len(log))
+            g = log[j]
+            assert int(g[0]) == (0 if kind == "layer" else 1) and int(g[1]) == idx, (j, g, d)
+            eps = logit_eps if logit_eps is not None else 1e-4
+            f_tol = 4.0 * eps + 1e-4 * (1 + np.abs(s_o))
+            assert np.all(np.abs(g[2:5] - s_o) <= f_tol), ("state", j, g[2:5], s_o)
+            q_tol = lip * float(np.max(f_tol)) + 1e-3 * (1 + np.max(np.abs(q_o)))
+            assert np.all(np.abs(g[5:7] - q_o) <= q_tol), ("Q", j, g[5:7], q_o)
+            if int(g[7]) != a_o:
+                assert abs(q_o[1] - q_o[0]) <= 2 * q_tol, ("action", j, q_o, g)
+                diverged = True
+                break
+        if not diverged:
+            assert len(log) == len(orc.decisions)
+            assert (rec.l, rec.k_eff) == (orc.l, orc.k_eff), (rec, orc.l, orc.k_eff)
+            n_same = 0
+            while n_same < orc.k_eff and rec.drafts[n_same] == orc.drafts[n_same]:
+                n_same += 1
+            if n_same < orc.k_eff:          # a near tie inside the draft argmax
+                zd = eng.logits(3)
+                rep.token(dt, rec.drafts[n_same], st.last_draft_logits[n_same])
+                diverged = True
+        if not diverged:
+            zv = eng.logits(0)
+            for j in range(orc.k_eff + 1):
+                rep.row(dt, zv[j], st.last_verify_logits[j])
+                gtok = int(np.argmax(zv[j]))
+                if gtok != orc.verify[j]:
+                    rep.token(dt, gtok, st.last_verify_logits[j])
+                    diverged = True
+                    break
+        if not diverged:
+            assert rec.accepted == orc.accepted and rec.emitted == orc.emitted
+            sl, pend, table = eng.lede_get_kv_state()
+            assert (sl, pend) == (orc.seq_len, st.pending) and table == orc.block_table
+            tr = eng.lede_get_trace()
+            assert len(tr) == len(st.trace.vals)
+            assert np.allclose(tr, np.array(st.trace.vals), atol=4 * (logit_eps or 1e-4) + 1e-4)
+        else:
+            rep.substitutions += 1
+            eng.lede_truncate(c0)
+            eng.lede_prefill([pending0] + orc.emitted[:-1])
+            eng.lede_set_pending(st.pending)
+            eng.lede_set_trace(np.array(st.trace.vals, dtype=np.float32))
+    return rep

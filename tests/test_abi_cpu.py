@@ -105,3 +105,24 @@ def test_sampling_entry_points_reject_bad_arguments(lib):
     assert lib.lede_op_sample(x, 16, 0.6, 0.5, None, None) == lede.LEDE_E_ARG
     u = (ctypes.c_float * lede.SAMPLE_STRIDE)()
     assert lib.lede_step_sampled(None, None, 0, 4, 0.6, u, None, None) == lede.LEDE_E_ARG
+
+
+def test_exit_policy_config_and_entry_points(lib):
+    from paper_2606_03113_amd import lede
+    wb0, wb1 = ctypes.c_size_t(), ctypes.c_size_t()
+    cfg = lede.make_config(TINY, 128)
+    assert lib.lede_region_bytes(ctypes.byref(cfg), ctypes.byref(wb0), None, None) == 0
+    cfg = lede.make_config(TINY, 128, exit_hidden=16)
+    assert lib.lede_region_bytes(ctypes.byref(cfg), ctypes.byref(wb1), None, None) == 0
+    assert wb1.value >= wb0.value + 4 * (16 * 3 + 16 + 2 * 16 + 2)
+    for bad in (-1, 1025):
+        cfg = lede.make_config(TINY, 128, exit_hidden=bad)
+        assert lib.lede_region_bytes(ctypes.byref(cfg), None, None, None) == lede.LEDE_E_UNSUPPORTED
+    m = shrink(TINY, qnet_hidden=0, exits=(3, 2))
+    cfg = lede.make_config(m, 128, exit_hidden=8)       # candidates must ascend
+    assert lib.lede_region_bytes(ctypes.byref(cfg), None, None, None) == lede.LEDE_E_UNSUPPORTED
+    rec = lede.LedeStepRecord()
+    assert lib.lede_step_policy(None, 4, None, ctypes.byref(rec)) == lede.LEDE_E_ARG
+    assert lib.lede_set_trace(None, None, 0, None) == lede.LEDE_E_ARG
+    n = ctypes.c_int32()
+    assert lib.lede_get_trace(None, None, ctypes.byref(n), None) == lede.LEDE_E_ARG
