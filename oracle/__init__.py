@@ -8,7 +8,8 @@ never used as a fallback for it.
 ``lede_oracle.c`` holds the decoder arithmetic in fp64; ``model.py`` holds the
 decoding loop: greedy autoregressive decoding (the plain definition the
 self-speculative loop must reproduce), the draft / verify / accept / commit
-step, the page allocator, the Q-network, the reward and the run metrics.
+step, the page allocator, the Q-network, the reward and the run metrics;
+``dqn.py`` holds the offline optimisation of the exit policy's Q-network.
 """
 from .build import build, library_path  # noqa: F401
 from .model import (OracleDecoder, Pager, StepRecord, accept_length, greedy_ar,  # noqa: F401
