@@ -102,6 +102,53 @@ def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
                       "bf16 values, no oracle prefill); %.1f s" % (steps, l, k, wl.name, P, el)}
 
 
+def dqn_leg(torch, li, n_updates=2000, H=16, B=32):
+    """Learning updates of the exit policy's trainer with the paper's
+    hyperparameters (mini-batch 32, n = 3, gamma = 0.99, Adam 6.25e-5, noisy
+    layers sigma0 = 0.1, a target copy every 512 updates) on a ring of 8192
+    synthetic transitions; inputs resident on the device."""
+    from paper_2606_03113_amd import Dqn
+    q = Dqn(hidden=H, capacity=1 << 16, batch=B)
+    q.lede_dqn_init(li.dqn_init_uniforms(H))
+    q.lede_dqn_push(li.dqn_transitions(8192))
+    ins = [li.dqn_update_inputs(i, H, B) for i in range(n_updates)]
+    u = torch.from_numpy(np.stack([a for a, _ in ins])).cuda()
+    nz = torch.from_numpy(np.stack([b for _, b in ins])).cuda()
+    for i in range(20):
+        q.lede_dqn_update(u[i], nz[i], want_loss=False)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(n_updates):
+        q.lede_dqn_update(u[i], nz[i], want_loss=False)
+        if i % 512 == 511:
+            q.lede_dqn_sync_target()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    loss = q.lede_dqn_update(u[0], nz[0])
+    q.close()
+    return {"updates_per_s": round(n_updates / (ms / 1e3), 1), "us_per_update": round(1e3 * ms / n_updates, 2),
+            "hidden": H, "batch": B, "n_step": 3, "replay": 8192, "last_loss": round(loss, 5),
+            "bound": "latency (one block per update; host launch included)"}
+
+
+def dqn_oracle_rate(li, budget_s=3.0, H=16, B=32):
+    """The oracle trainer's learning updates per second on the same inputs."""
+    from oracle import dqn as od
+    tr = od.Trainer(od.Hyper(hidden=H, batch=B), 1 << 16, li.dqn_init_uniforms(H).astype(np.float64))
+    for row in li.dqn_transitions(8192).astype(np.float64):
+        tr.replay.push(row[:3], int(row[3]), row[4], bool(row[5]))
+    t0 = time.time()
+    n = 0
+    while n < 5 or time.time() - t0 < budget_s:
+        u, nz = li.dqn_update_inputs(n, H, B)
+        tr.update(u.astype(np.float64), nz[0].astype(np.float64), nz[1].astype(np.float64))
+        n += 1
+    return round(n / (time.time() - t0), 1)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -112,6 +159,7 @@ def main():
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--prof-steps", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dqn", action="store_true", help="skip the policy-trainer update timing")
     ap.add_argument("--graphs", type=int, default=0)
     ap.add_argument("--policy", choices=["fixed", "paper"], default="fixed",
                     help="paper: the paper's exit policy (seeded random exit Q-network) chooses l* and k per step")
@@ -327,9 +375,14 @@ def main():
                            "frac": round(max(probe.values()) / HBM_PEAK_GBPS, 4),
                            "bytes": probe_bytes, "by_grid": {str(g): round(v, 1) for g, v in probe.items()}},
     }
+    if not args.no_dqn:
+        log("policy trainer updates ...")
+        out["dqn"] = dqn_leg(torch, li)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(wl, weights, qnet, first)
+        if "dqn" in out:
+            out["dqn"]["oracle_updates_per_s"] = dqn_oracle_rate(li)
     print(json.dumps(out), flush=True)
 
 

@@ -233,6 +233,100 @@ int lede_step_policy(lede_ctx* ctx, int32_t n_remaining, void* stream, lede_step
 int lede_set_trace(lede_ctx* ctx, const float* values, int32_t n, void* stream);
 int lede_get_trace(lede_ctx* ctx, float* values /* [20] */, int32_t* n, void* stream);
 
+/* ---- offline optimisation of the exit policy's Q-network ------------------
+ * Section 3.2 (experience replay, n-step TD error to a target network,
+ * greedy target action) with the training setup of Section 4.1 (Adam,
+ * factorised Gaussian noisy layers, mini-batches, periodic target copies).
+ * The network is the exit policy's 3 -> H -> 2 MLP; every weight w of it is
+ * mu + sigma * f(eps_out) f(eps_in), f(x) = sgn(x) sqrt(|x|) (NoisyNet,
+ * factorised), with standard normals supplied by the caller.
+ *
+ * Device memory, caller-owned, lede_dqn_region_bytes bytes (256-aligned):
+ * online parameters [mu, sigma] (2P floats, P = 6H + 2, each set laid out W1
+ * [H][3], b1 [H], W2 [2][H], b2 [2]), target parameters, Adam moments m and
+ * v, and the replay ring (capacity slots of 8 floats: state C_5, H, C_trace,
+ * action, reward, terminal, 2 unused).  The handle keeps host-side counters
+ * (ring head and count, Adam step t); calls are stream-ordered and a handle
+ * is not thread-safe.  Every entry returns a lede_status; errors leave the
+ * handle unchanged and set lede_dqn_last_error. */
+typedef struct lede_dqn lede_dqn;
+typedef struct {
+  int32_t hidden;    /* H, 1..128 (the exit policy's exit_qnet_hidden) */
+  int32_t capacity;  /* replay slots, 2..2^24 */
+  int32_t batch;     /* mini-batch, 1..256, batch * hidden <= 4096 */
+  int32_t n_step;    /* n of the n-step target, 1..16 */
+  float gamma;       /* discount, [0, 1] */
+  float lr;          /* Adam step size, > 0 */
+  float beta1, beta2;  /* Adam moment decays, [0, 1) */
+  float adam_eps;    /* Adam epsilon, > 0 */
+  float sigma0;      /* noisy-layer initial scale, >= 0 */
+} lede_dqn_config;
+
+/* Bytes of the device region for cfg; 0 for an invalid cfg. */
+size_t lede_dqn_region_bytes(const lede_dqn_config* cfg);
+/* Handle over a caller region of at least lede_dqn_region_bytes (device,
+ * 256-byte aligned).  Allocates host memory only.  LEDE_E_ARG on a null
+ * pointer, a small or misaligned region; LEDE_E_UNSUPPORTED on sizes outside
+ * the ranges above. */
+int lede_dqn_create(const lede_dqn_config* cfg, void* region, size_t bytes, lede_dqn** out);
+void lede_dqn_destroy(lede_dqn* q);
+const char* lede_dqn_last_error(const lede_dqn* q);
+
+/* Initialisation (NoisyNet, factorised): mu = (2u - 1) / sqrt(p) from the
+ * device uniforms u [P] in [0, 1), sigma = sigma0 / sqrt(p), p the layer's
+ * fan-in (3, then H); target = online; Adam moments zero, t = 0; the ring is
+ * emptied. */
+int lede_dqn_init(lede_dqn* q, const float* u, void* stream);
+
+/* Appends n >= 0 caller transitions (device [n][6] floats: state (3),
+ * action 0 / 1, reward, terminal 0 / 1) in order; when n exceeds the
+ * capacity only the last capacity land.  The newest overwrite the oldest. */
+int lede_dqn_push(lede_dqn* q, const float* transitions, int32_t n, void* stream);
+
+/* Appends the decisions of ctx's last lede_step_policy as transitions, in
+ * decision order (Section 3.3): the state of the decision, the executed
+ * action (the last candidate layer's forced exit is stored as exit), and the
+ * Section 3.1.3 reward with lambda = (L - l*) / L: 'continue' -0.01; an exit
+ * at a candidate layer scores draft 1, an exit after a further draft pass
+ * scores the draft it keeps, +1 + lambda when that draft is among the
+ * accepted ones, -2 + lambda otherwise.  The next transition's state is the
+ * successor state.  episode_end != 0 marks the newest stored transition
+ * terminal (the generation ended).  Must follow the policy step before any
+ * other step, prefill, truncation or set_pending on ctx (LEDE_E_STATE
+ * otherwise).  ctx and q share the device and stream order. */
+int lede_dqn_record(lede_dqn* q, lede_ctx* ctx, int32_t episode_end, void* stream);
+
+/* Marks the newest stored transition terminal (no-op on an empty ring). */
+int lede_dqn_end_episode(lede_dqn* q, void* stream);
+
+/* One learning update.  u: device [batch] uniforms, each m / 2^24 with an
+ * integer m; sample b is the transition at position floor(m_b * n_valid /
+ * 2^24) of the stored ones, oldest first, n_valid = count - n_step (a
+ * transition is sampled once its n successors are stored; LEDE_E_STATE when
+ * n_valid < 1).  noise: device [2][2H + 5] standard normals, eps_in (3) and
+ * eps_out (H) of layer 1 then eps_in (H) and eps_out (2) of layer 2, for the
+ * online network and then the target network.  Target y = sum_{k<n} gamma^k
+ * r_{t+k} (stopping after a terminal transition) + gamma^n max_a'
+ * Qbar(s_{t+n}, a') (only without a terminal); loss = mean (Q(s_t, a_t) -
+ * y)^2; Adam (t += 1) on every mu and sigma.  loss (nullable host pointer)
+ * receives the loss, which synchronises the stream. */
+int lede_dqn_update(lede_dqn* q, const float* u, const float* noise, void* stream, float* loss);
+
+/* Copies the online parameters into the target network. */
+int lede_dqn_sync_target(lede_dqn* q, void* stream);
+
+/* Writes the acting network into ctx's exit-policy Q-network: mu + sigma *
+ * noise for noise = device [2H + 5] standard normals (exploration), or the
+ * means for noise = NULL.  LEDE_E_STATE when ctx has no exit policy of width
+ * H. */
+int lede_dqn_act(lede_dqn* q, lede_ctx* ctx, const float* noise, void* stream);
+
+/* Host read-back (synchronises): which = 0 online [mu, sigma], 1 target,
+ * 2 Adam m, 3 Adam v (2P floats each); 4 the stored transitions, oldest
+ * first, 6 floats each.  *count receives the number of floats (or
+ * transitions for 4); LEDE_E_ARG when cap_floats is too small. */
+int lede_dqn_read(lede_dqn* q, int32_t which, float* host, size_t cap_floats, int32_t* count, void* stream);
+
 /* Committed KV length, pending token and the page table (host copies). */
 int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t* block_table,
                       int32_t cap, int32_t* n_table);

@@ -22,7 +22,7 @@ import threading
 
 import numpy as np
 
-from .configs import (PAGE_SIZE, SAMPLE_SLOTS, SAMPLE_STRIDE, SEED_PROMPT, SEED_QNET, SEED_SAMPLE,
+from .configs import (PAGE_SIZE, SAMPLE_SLOTS, SAMPLE_STRIDE, SEED_DQN, SEED_PROMPT, SEED_QNET, SEED_SAMPLE,
                       SEED_SCHEDULE, SEED_WEIGHTS, WEIGHT_STD, WORKLOADS, ModelConfig, Workload, shrink)
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -41,6 +41,13 @@ STREAM_SCHED_L = 30
 STREAM_SCHED_K = 31
 STREAM_SAMPLE = 40
 STREAM_EXIT_QNET = 12
+STREAM_DQN_STATE = 50
+STREAM_DQN_ACTION = 51
+STREAM_DQN_REWARD = 52
+STREAM_DQN_DONE = 53
+STREAM_DQN_BATCH = 54
+STREAM_DQN_NOISE = 55
+STREAM_DQN_INIT = 56
 LAYER_BASE = 1000
 LAYER_STRIDE = 16
 LAYER_TENSORS = {"wq": 1, "wk": 2, "wv": 3, "wo": 4, "wg": 6, "wu": 7, "wd": 8}
@@ -191,6 +198,31 @@ def exit_qnet_weights(hidden: int = 16, seed: int = SEED_QNET, std: float = 0.5)
         "w2": normal(seed, STREAM_EXIT_QNET + 2, 2 * hidden, std, "f32").reshape(2, hidden),
         "b2": np.zeros(2, dtype=np.float32),
     }
+
+
+def dqn_transitions(n: int, seed: int = SEED_DQN, p_done: float = 0.15, offset: int = 0) -> np.ndarray:
+    """[n][6] float32 synthetic transitions: state (3, N(0, 2^2)), action
+    0 / 1, reward N(0, 1), terminal with probability p_done."""
+    t = np.zeros((n, 6), dtype=np.float32)
+    t[:, :3] = normal(seed, STREAM_DQN_STATE, 3 * n, 2.0, "f32", offset=3 * offset).reshape(n, 3)
+    t[:, 3] = uniform_int(seed, STREAM_DQN_ACTION, n, 0, 1, offset=offset)
+    t[:, 4] = normal(seed, STREAM_DQN_REWARD, n, 1.0, "f32", offset=offset)
+    t[:, 5] = uniform01(seed, STREAM_DQN_DONE, n, offset=offset) < p_done
+    return t
+
+
+def dqn_init_uniforms(hidden: int, seed: int = SEED_DQN) -> np.ndarray:
+    """Uniforms of one parameter set of the 3 -> H -> 2 network (6H + 2)."""
+    return uniform01(seed, STREAM_DQN_INIT, 6 * hidden + 2)
+
+
+def dqn_update_inputs(i: int, hidden: int, batch: int, seed: int = SEED_DQN):
+    """Inputs of learning update i: batch uniforms and the standard normals of
+    the online and the target network's noise ([2][2H + 5])."""
+    nc = 2 * hidden + 5
+    u = uniform01(seed, STREAM_DQN_BATCH, batch, offset=i * batch)
+    noise = normal(seed, STREAM_DQN_NOISE, 2 * nc, 1.0, "f32", offset=i * 2 * nc).reshape(2, nc)
+    return u, noise
 
 
 def prompt(w: Workload, seed: int = SEED_PROMPT, length: int | None = None) -> np.ndarray:

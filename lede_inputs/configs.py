@@ -17,6 +17,7 @@ SEED_PROMPT = 1
 SEED_SCHEDULE = 2
 SEED_QNET = 3
 SEED_SAMPLE = 4          # uniforms of speculative sampling
+SEED_DQN = 5             # policy-trainer inputs: transitions, mini-batch uniforms, noise
 SAMPLE_SLOTS = 16        # per step: draft uniforms [0, 16), acceptance uniforms [16, 32), residual / bonus [32]
 SAMPLE_STRIDE = 2 * SAMPLE_SLOTS + 1
 

@@ -1,6 +1,6 @@
 // Internal interface between the runtime (runtime.cpp) and the gfx950
 // kernels (linear.hip, norm.hip, attention.hip, accept.hip, policy.hip,
-// misc.hip).  Not part of the public C ABI.
+// dqn.hip, misc.hip).  Not part of the public C ABI.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stddef.h>
@@ -88,6 +88,46 @@ struct TracePushArgs {
   float* trace; int32_t* trace_state;              // state[0] = count, state[1] = next slot
 };
 
+// Offline optimisation of the exit policy's Q-network (3 -> H -> 2 MLP with
+// factorised noisy layers).  A parameter set is one flat fp32 vector: W1
+// [H][3], b1 [H], W2 [2][H], b2 [2] (P = 6H + 2 entries); theta = [mu, sigma]
+// (2P).  One network's noise is 3 + 2H + 2 standard normals: eps_in and
+// eps_out of layer 1, then of layer 2.  A replay slot is 8 floats: state (3),
+// action, reward, terminal, 2 unused.
+constexpr int DQN_SLOT = 8, DQN_MAX_HIDDEN = 128, DQN_MAX_BATCH = 256, DQN_MAX_BH = 4096, DQN_MAX_N = 16;
+constexpr int DQN_THREADS = 256;
+__host__ __device__ inline int dqn_params(int H) { return 6 * H + 2; }
+__host__ __device__ inline int dqn_noise(int H) { return 2 * H + 5; }
+struct DqnInitArgs {
+  const float* u; int H; float sigma0;
+  float* theta; float* target; float* m; float* v;
+};
+struct DqnUpdateArgs {
+  float* theta; const float* target; float* m; float* v;
+  const float* ring; int capacity, oldest, n_valid;
+  const float* u;                  // [B] uniforms m / 2^24
+  const float* noise;              // [2][3 + 2H + 2]: online, then target
+  int H, B, n;
+  float gamma, gamma_n, lr, beta1, beta2, eps, bc1, bc2;  // bc = 1 - beta^t
+  float* loss_out;                 // [1]
+};
+struct DqnRecordArgs {
+  const float* log; int n_dec;     // POLICY_LOG floats per decision
+  int l_star, accepted;
+  float r_accept, r_reject, r_continue;
+  float* ring; int capacity, head;
+  int end_episode, prev_newest;    // prev_newest: slot marked terminal when n_dec = 0 (-1: none)
+};
+struct DqnPushArgs {
+  const float* src; int n;         // [n][6]: state (3), action, reward, terminal
+  float* ring; int capacity, head;
+};
+struct DqnActArgs {
+  const float* theta; const float* noise;  // noise may be null: the means
+  int H;
+  float *w1, *b1, *w2, *b2;
+};
+
 // Launchers (one per kernel family, next to its kernels).  All return
 // hipError_t of the launch.
 hipError_t launch_norm(int dtype, const NormArgs& a, hipStream_t s);
@@ -104,6 +144,12 @@ hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
 hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t s,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
+hipError_t launch_dqn_init(const DqnInitArgs& a, hipStream_t s);
+hipError_t launch_dqn_update(const DqnUpdateArgs& a, hipStream_t s);
+hipError_t launch_dqn_record(const DqnRecordArgs& a, hipStream_t s);
+hipError_t launch_dqn_push(const DqnPushArgs& a, hipStream_t s);
+hipError_t launch_dqn_copy(const float* src, float* dst, int n, hipStream_t s);
+hipError_t launch_dqn_act(const DqnActArgs& a, hipStream_t s);
 
 
 }  // namespace lede

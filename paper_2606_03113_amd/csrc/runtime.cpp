@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "../../include/lede.h"
+#include "ctx_view.h"
 #include "kernels.h"
 
 using namespace lede;
@@ -129,7 +130,7 @@ Layout make_layout(const lede_config* c) {
   o.dstats = take(2 * SAMPLE_SLOTS * 4);
   o.trace = take(POLICY_TRACE * 4);
   o.trace_state = take(4 * 4);
-  o.pol_out = take(POLICY_LOG * 4);
+  o.pol_out = take((size_t)(c->n_exits + POLICY_MAX_DRAFT) * POLICY_LOG * 4);
   o.wsbytes = off;
 
   o.kv_half = align256((size_t)o.L * o.n_pages * o.nkv * PAGE * o.hd * o.es);
@@ -156,6 +157,8 @@ struct lede_ctx {
   float* unif_h = nullptr;      // pinned staging of a sampled step's uniforms
   float* trace_h = nullptr;     // pinned staging of the confidence trace and policy decisions
   std::vector<float> policy_log;  // decisions of the last exit-policy step, POLICY_LOG floats each
+  // the last step was an exit-policy step whose decision log (device) is intact
+  int policy_valid = 0, policy_l = 0, policy_a = 0;
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
@@ -616,6 +619,7 @@ int read_record(lede_ctx* c, hipStream_t s) {
 
 // Apply a finished verify (record read back) to the host mirror.
 void commit_host(lede_ctx* c) {
+  c->policy_valid = 0;
   c->seq_len = c->record_h[2];
   c->pending = c->record_h[3];
   truncate_pages(c, c->seq_len);
@@ -771,6 +775,7 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c->lo.V) return fail(c, LEDE_E_ARG, "token %d out of range", tokens[i]);
   hipStream_t s = S_(stream);
+  c->policy_valid = 0;
   const int c0 = c->seq_len;
   const size_t saved_table = c->table.size();
   int rc = ensure_pages(c, c0 + n);
@@ -813,6 +818,7 @@ int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
   if (token < 0 || token >= c->lo.V) return fail(c, LEDE_E_ARG, "token out of range");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   hipStream_t s = S_(stream);
+  c->policy_valid = 0;
   HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, token, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
   c->pending = token;
@@ -823,6 +829,7 @@ int lede_truncate(lede_ctx* c, int32_t new_len, void* stream) {
   if (!c) return LEDE_E_ARG;
   if (new_len < 0 || new_len > c->seq_len) return fail(c, LEDE_E_ARG, "new_len %d not in [0, %d]", new_len, c->seq_len);
   hipStream_t s = S_(stream);
+  c->policy_valid = 0;
   truncate_pages(c, new_len);
   c->drafted_k = -1;
   int rc = upload_table(c, s);
@@ -854,6 +861,7 @@ int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts)
   hipStream_t s = S_(stream);
   int rc = draft_impl(c, l, k, s);
   if (rc) return rc;
+  c->policy_valid = 0;
   if (drafts) {
     HIP_CHECK(c, hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), 32 * 8, hipMemcpyDeviceToHost, s));
     HIP_CHECK(c, hipStreamSynchronize(s));
@@ -1037,6 +1045,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
   rec->q_action = -1;
   rec->q_max = NAN;
   c->policy_log.clear();
+  c->policy_valid = 0;
   const int c0 = c->seq_len;
   const int k_lim = std::max(0, std::min(std::min(POLICY_MAX_DRAFT, o.k_max), n_remaining - 1));
   int rc;
@@ -1046,9 +1055,11 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
   pa.vocab = o.V; pa.hidden = o.He;
   pa.w1 = c->W<float>(o.ew1); pa.b1 = c->W<float>(o.eb1); pa.w2 = c->W<float>(o.ew2); pa.b2 = c->W<float>(o.eb2);
   pa.trace = c->S<float>(o.trace); pa.trace_state = c->S<int32_t>(o.trace_state);
-  pa.out = c->S<float>(o.pol_out);
-  // one decision: the state of the head's logits, scored on the device, read back
+  float* log_dev = c->S<float>(o.pol_out);
+  // one decision: the state of the head's logits, scored on the device (kept in
+  // the device decision log), read back
   auto decide = [&](const float* logits, int kind, int index, int* action) -> int {
+    pa.out = log_dev + c->policy_log.size();
     pa.logits = logits; pa.kind = (float)kind; pa.index = (float)index;
     HIP_CHECK(c, launch_exit_policy(pa, s));
     HIP_CHECK(c, hipMemcpyAsync(c->trace_h, pa.out, POLICY_LOG * 4, hipMemcpyDeviceToHost, s));
@@ -1092,6 +1103,9 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
   commit_host(c);
   if ((rc = prof_fold(c))) return rc;
   const int a = c->record_h[0];
+  c->policy_valid = 1;
+  c->policy_l = l_star;
+  c->policy_a = a;
   rec->l = l_star;
   rec->k_req = POLICY_MAX_DRAFT;
   rec->k_eff = k;
@@ -1266,3 +1280,31 @@ int lede_op_read_probe(const void* src, size_t bytes, uint32_t* sink, int32_t gr
 }
 
 }  // extern "C"
+
+// ---- views for the policy trainer (dqn.cpp) ----------------------------------------
+
+namespace lede {
+
+int policy_step_take(lede_ctx* c, PolicyStepView* v) {
+  if (!c->policy_valid) return LEDE_E_STATE;
+  c->policy_valid = 0;
+  v->log = c->S<float>(c->lo.pol_out);
+  v->n_dec = (int)(c->policy_log.size() / POLICY_LOG);
+  v->l_star = c->policy_l;
+  v->accepted = c->policy_a;
+  v->n_layers = c->lo.L;
+  return LEDE_OK;
+}
+
+int exit_weights_view(lede_ctx* c, ExitWeightsView* v) {
+  const Layout& o = c->lo;
+  if (!o.He) return LEDE_E_STATE;
+  v->w1 = c->W<float>(o.ew1);
+  v->b1 = c->W<float>(o.eb1);
+  v->w2 = c->W<float>(o.ew2);
+  v->b2 = c->W<float>(o.eb2);
+  v->hidden = o.He;
+  return LEDE_OK;
+}
+
+}  // namespace lede

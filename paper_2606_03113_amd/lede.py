@@ -66,7 +66,9 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
             "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
             "lede_op_read_probe", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
-            "lede_get_trace"]
+            "lede_get_trace", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
+            "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
+            "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read"]
 SAMPLE_SLOTS = 16
 SAMPLE_STRIDE = 33
 
@@ -113,11 +115,35 @@ def load(path: str = LIB_PATH):
     L.lede_step_policy.argtypes = [vp, i32, vp, P(LedeStepRecord)]
     L.lede_set_trace.argtypes = [vp, P(ctypes.c_float), i32, vp]
     L.lede_get_trace.argtypes = [vp, P(ctypes.c_float), P(i32), vp]
+    fp = P(ctypes.c_float)
+    L.lede_dqn_region_bytes.argtypes = [P(LedeDqnConfig)]
+    L.lede_dqn_region_bytes.restype = sz
+    L.lede_dqn_create.argtypes = [P(LedeDqnConfig), vp, sz, P(vp)]
+    L.lede_dqn_destroy.argtypes = [vp]
+    L.lede_dqn_destroy.restype = None
+    L.lede_dqn_last_error.argtypes = [vp]
+    L.lede_dqn_last_error.restype = ctypes.c_char_p
+    L.lede_dqn_init.argtypes = [vp, vp, vp]
+    L.lede_dqn_push.argtypes = [vp, vp, i32, vp]
+    L.lede_dqn_record.argtypes = [vp, vp, i32, vp]
+    L.lede_dqn_end_episode.argtypes = [vp, vp]
+    L.lede_dqn_update.argtypes = [vp, vp, vp, vp, fp]
+    L.lede_dqn_sync_target.argtypes = [vp, vp]
+    L.lede_dqn_act.argtypes = [vp, vp, vp, vp]
+    L.lede_dqn_read.argtypes = [vp, i32, fp, sz, P(i32), vp]
     for name in EXPORTED:
-        if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes"):
+        if name not in ("lede_destroy", "lede_last_error", "lede_op_tiled_bytes", "lede_dqn_region_bytes",
+                        "lede_dqn_destroy", "lede_dqn_last_error"):
             getattr(L, name).restype = ctypes.c_int
     _lib = L
     return L
+
+
+class LedeDqnConfig(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("capacity", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("n_step", ctypes.c_int32), ("gamma", ctypes.c_float), ("lr", ctypes.c_float),
+                ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("adam_eps", ctypes.c_float),
+                ("sigma0", ctypes.c_float)]
 
 
 class LedeError(RuntimeError):
@@ -311,7 +337,7 @@ class Engine:
     def policy_log(self) -> np.ndarray:
         """Decisions of the last lede_step_policy: rows of (kind, layer / draft,
         C_5, H, C_trace, Q(continue), Q(exit), action)."""
-        out, rows = self.lede_debug_read(4, 64 * 8)
+        out, rows = self.lede_debug_read(4, (64 + 12) * 8)
         return out[:rows * 8].reshape(rows, 8)
 
     def lede_set_trace(self, values):
@@ -411,3 +437,103 @@ def op_sample(logits, temperature: float, u: float) -> int:
     if rc:
         raise LedeError(rc, "op_sample")
     return tok.value
+
+
+def dqn_noise_count(hidden: int) -> int:
+    """Standard normals one network draw takes: eps_in, eps_out of both layers."""
+    return 2 * hidden + 5
+
+
+def dqn_param_count(hidden: int) -> int:
+    """Entries of [mu, sigma] of the 3 -> H -> 2 network."""
+    return 2 * (6 * hidden + 2)
+
+
+class Dqn:
+    """A liblede policy trainer (lede_dqn_*) over a torch-allocated region."""
+
+    def __init__(self, hidden: int = 16, capacity: int = 1 << 16, batch: int = 32, n_step: int = 3,
+                 gamma: float = 0.99, lr: float = 6.25e-5, beta1: float = 0.9, beta2: float = 0.999,
+                 adam_eps: float = 1.5e-4, sigma0: float = 0.1, device: int = 0):
+        import torch
+        self.torch = torch
+        self.L = load()
+        self.cfg = LedeDqnConfig(hidden, capacity, batch, n_step, gamma, lr, beta1, beta2, adam_eps, sigma0)
+        nbytes = self.L.lede_dqn_region_bytes(ctypes.byref(self.cfg))
+        if nbytes == 0:
+            raise LedeError(LEDE_E_ARG, "invalid trainer configuration")
+        self.device = torch.device("cuda", device)
+        self.region = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        h = ctypes.c_void_p()
+        rc = self.L.lede_dqn_create(ctypes.byref(self.cfg), self.region.data_ptr(), nbytes, ctypes.byref(h))
+        if rc != LEDE_OK:
+            raise LedeError(rc, "lede_dqn_create")
+        self.q = h
+
+    @property
+    def stream(self):
+        return ctypes.c_void_p(self.torch.cuda.current_stream(self.device).cuda_stream)
+
+    def _check(self, rc: int):
+        if rc != LEDE_OK:
+            raise LedeError(rc, self.L.lede_dqn_last_error(self.q).decode())
+
+    def _dev(self, a):
+        """A device fp32 copy of a host array (kept alive by the caller)."""
+        return self.torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.device)
+
+    def close(self):
+        if getattr(self, "q", None):
+            self.L.lede_dqn_destroy(self.q)
+            self.q = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def lede_dqn_init(self, u):
+        d = self._dev(u)
+        self._check(self.L.lede_dqn_init(self.q, d.data_ptr(), self.stream))
+        self.torch.cuda.current_stream(self.device).synchronize()
+
+    def lede_dqn_push(self, transitions):
+        t = np.ascontiguousarray(transitions, dtype=np.float32).reshape(-1, 6)
+        d = self._dev(t)
+        self._check(self.L.lede_dqn_push(self.q, d.data_ptr(), len(t), self.stream))
+        self.torch.cuda.current_stream(self.device).synchronize()
+
+    def lede_dqn_record(self, engine, episode_end: bool = False):
+        self._check(self.L.lede_dqn_record(self.q, engine.ctx, int(episode_end), self.stream))
+
+    def lede_dqn_end_episode(self):
+        self._check(self.L.lede_dqn_end_episode(self.q, self.stream))
+
+    def lede_dqn_update(self, u, noise, want_loss: bool = True):
+        """u: [batch] uniforms m / 2^24, noise: [2][2H + 5] normals, host
+        arrays or device tensors; returns the loss (or None)."""
+        t = self.torch
+        ud = u if isinstance(u, t.Tensor) else self._dev(u)
+        nd = noise if isinstance(noise, t.Tensor) else self._dev(noise)
+        loss = ctypes.c_float()
+        self._check(self.L.lede_dqn_update(self.q, ud.data_ptr(), nd.data_ptr(), self.stream,
+                                           ctypes.byref(loss) if want_loss else None))
+        return loss.value if want_loss else None
+
+    def lede_dqn_sync_target(self):
+        self._check(self.L.lede_dqn_sync_target(self.q, self.stream))
+
+    def lede_dqn_act(self, engine, noise=None):
+        nd = None if noise is None else self._dev(noise)
+        self._check(self.L.lede_dqn_act(self.q, engine.ctx, None if nd is None else nd.data_ptr(), self.stream))
+        self.torch.cuda.current_stream(self.device).synchronize()
+
+    def lede_dqn_read(self, which: int) -> np.ndarray:
+        """0 online [mu, sigma], 1 target, 2 Adam m, 3 Adam v; 4 transitions [count][6]."""
+        cap = dqn_param_count(self.cfg.hidden) if which < 4 else self.cfg.capacity * 6
+        out = np.zeros(cap, dtype=np.float32)
+        n = ctypes.c_int32()
+        self._check(self.L.lede_dqn_read(self.q, which, out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), cap,
+                                         ctypes.byref(n), self.stream))
+        return out[:n.value] if which < 4 else out[:n.value * 6].reshape(n.value, 6)
