@@ -44,9 +44,17 @@ def pass_bytes(m, l, c):
     return l * m.layer_weight_bytes() + m.head_weight_bytes() + l * (c + 1) * kv
 
 
-def verify_bytes(m, k, c):
+def verify_bytes(m, k, c, from_layer=0):
+    """Algorithmic bytes of the verify pass of k drafts at KV length c, from
+    layer from_layer (verify reuse) or from the embedding."""
     kv = m.kv_bytes_per_token_layer()
-    return m.n_layers * m.layer_weight_bytes() + m.head_weight_bytes() + m.n_layers * (c + k + 1) * kv
+    n = m.n_layers - from_layer
+    return n * m.layer_weight_bytes() + m.head_weight_bytes() + n * (c + k + 1) * kv
+
+
+def extend_bytes(m, l, c, k):
+    """Verify reuse: the last draft's pass through layers 1..l (no head)."""
+    return l * m.layer_weight_bytes() + l * (c + k + 1) * m.kv_bytes_per_token_layer()
 
 
 def kernel_source_sha():
@@ -160,6 +168,8 @@ def main():
     ap.add_argument("--prof-steps", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dqn", action="store_true", help="skip the policy-trainer update timing")
+    ap.add_argument("--verify-reuse", action="store_true",
+                    help="verify from the exit layer on the draft passes' hidden states and KV")
     ap.add_argument("--graphs", type=int, default=0)
     ap.add_argument("--policy", choices=["fixed", "paper"], default="fixed",
                     help="paper: the paper's exit policy (seeded random exit Q-network) chooses l* and k per step")
@@ -205,6 +215,10 @@ def main():
     if paper:
         eng.load_exit_qnet(li.exit_qnet_weights(16))
     eng.lede_set_options(args.graphs, 0)
+    if args.verify_reuse:
+        if args.graphs:
+            sys.exit("steps with verify reuse run eagerly")
+        eng.lede_set_verify_reuse(True)
     log("weights resident (%.1f GB arena)  %.1f s" % (eng.region_bytes[0] / 1e9, time.time() - t0))
     first = eng.lede_prefill(prompt)
     log("prefill %d tokens done  %.1f s" % (wl.prompt_len, time.time() - t0))
@@ -320,7 +334,11 @@ def main():
     for r in phase_recs:
         c = r.seq_len - r.accepted - 1  # KV length when the step started
         db += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff)) + (m.qnet_bytes() if log_q else 0)
-        vb += verify_bytes(m, r.k_eff, c)
+        if args.verify_reuse and r.k_eff:
+            db += extend_bytes(m, r.l, c, r.k_eff)
+            vb += verify_bytes(m, r.k_eff, c, r.l)
+        else:
+            vb += verify_bytes(m, r.k_eff, c)
     acc_tokens = sum(len(r.emitted) for r in recs)
     accepted = sum(r.accepted for r in recs)
     drafted = sum(r.k_eff for r in recs)
@@ -347,7 +365,7 @@ def main():
                                 (list(m.exits),) if paper else
                                 "static exit l=%d, draft k=%d, Q-network logged" % (l, k)),
                    "batch": 1, "prompt_len": wl.prompt_len, "exit_layer": l, "draft_len": k,
-                   "graphs": bool(args.graphs),
+                   "graphs": bool(args.graphs), "verify_reuse": bool(args.verify_reuse),
                    "acceptance": ("speculative sampling, T=%g" % args.temperature if args.temperature > 0
                                   else "greedy"),
                    "policy": "paper exit policy (random exit Q-network)" if paper else "fixed"},

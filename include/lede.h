@@ -148,6 +148,22 @@ int lede_set_free_list(lede_ctx* ctx, const int32_t* order, int32_t n);
  * and the Q-values for lede_debug_read. */
 int lede_set_options(lede_ctx* ctx, int32_t use_graphs, int32_t debug);
 
+/* Verify reuse (the self-speculative decoding the paper builds on, Section
+ * 4.1 and Section 2.2: the draft layers are the model's own first layers).
+ * With enable != 0, the verify of a step with k > 0 drafts at exit layer l*
+ * runs only layers l*+1..L, on the layer-l* hidden states of rows [pending,
+ * d_1 .. d_k]: the draft passes leave those of the pending token and d_1 ..
+ * d_{k-1}, and one more one-row pass takes d_k through layers 1..l* (the
+ * exit policy's last pass already does when it ended drafting); the KV the
+ * draft passes wrote below l* is kept.  At batch 1 this reads the same weight
+ * bytes as a full verify and saves FLOPs and launches.  The verify rows'
+ * layers up to l* then come from the one-row kernels, so committed tokens
+ * equal greedy decoding up to rounding, not bit for bit.  Steps with reuse
+ * run eagerly (no graphs).  Applies to lede_step, lede_step_sampled,
+ * lede_step_policy and lede_verify.  LEDE_E_STATE while a draft is
+ * outstanding. */
+int lede_set_verify_reuse(lede_ctx* ctx, int32_t enable);
+
 /* Append n prompt tokens (host int32, each in [0, vocab)) at positions
  * seq_len .. seq_len+n-1 through all L layers, writing their K/V; the
  * argmax of the last row becomes the pending token and is returned in

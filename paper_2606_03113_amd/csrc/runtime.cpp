@@ -161,6 +161,7 @@ struct lede_ctx {
   int policy_valid = 0, policy_l = 0, policy_a = 0;
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
+  int verify_reuse = 0;  // verify from the exit layer on the draft passes' hidden states and KV
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
@@ -370,16 +371,21 @@ LinearArgs base_linear(const lede_ctx* c) {
 // [l_begin, l_end).  Vector kernels for one row (draft path), matrix-core
 // kernels otherwise.  qnet_after: run the Q-network after this many layers
 // (0 = never).
+// Layers [l_begin, l_end) for M rows.  One-row (vec) passes keep their
+// residual in row vec_row of the h buffer (a draft pass i uses row i - 1, so
+// that the hidden states of a step's draft inputs stay available).
 int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_begin, int l_end, int qnet_after,
-               uint64_t* zero_slot, hipStream_t s) {
+               uint64_t* zero_slot, hipStream_t s, int vec_row = 0) {
   const Layout& o = c->lo;
   const int dt = o.dt;
+  float* hrow = c->S<float>(o.h) + (vec ? (size_t)vec_row * o.d : 0);
   for (int j = l_begin; j < l_end; ++j) {
     const auto& lw = o.lay[j];
     const bool first = j == 0;
     // attention block: [norm] + QKV (rotary, KV append)
     LinearArgs qa = base_linear(c);
     qa.M = M;
+    qa.h = hrow;
     qa.w = c->W<uint8_t>(lw.wqkv);
     qa.n_groups = (o.qd + 2 * o.kvd) / 16;
     qa.KT = k_tiles(dt, o.d);
@@ -428,6 +434,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 
     LinearArgs oa = base_linear(c);
     oa.M = M;
+    oa.h = hrow;
     oa.w = c->W<uint8_t>(lw.wo);
     oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
     oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
@@ -437,6 +444,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     // feed-forward block
     LinearArgs ga = base_linear(c);
     ga.M = M;
+    ga.h = hrow;
     ga.w = c->W<uint8_t>(lw.wgu);
     ga.n_groups = 2 * o.F / 16; ga.KT = k_tiles(dt, o.d); ga.K = o.d;
     ga.epi = EPI_SWIGLU; ga.act = c->S<void>(o.act); ga.ld_act = o.Fp;
@@ -454,6 +462,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 
     LinearArgs da = base_linear(c);
     da.M = M;
+    da.h = hrow;
     da.w = c->W<uint8_t>(lw.wd);
     da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
     da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
@@ -463,7 +472,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     if (qnet_after == j + 1 && o.H > 0) {
       NormArgs na{};
       na.M = 1; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
-      na.h = c->S<float>(o.h); na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
+      na.h = hrow; na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
       na.x = c->S<void>(o.qs); na.f32_out = 1;
       LAUNCH(LEDE_K_QNET, (double)o.d * 8, launch_norm(dt, na, s));
       LinearArgs la = base_linear(c);
@@ -483,10 +492,11 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 }
 
 // Shared final RMSNorm + LM head + argmax for rows [0, M) into keys[0..M).
-int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s) {
+int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s, int vec_row = 0) {
   const Layout& o = c->lo;
   LinearArgs ha = base_linear(c);
   ha.M = M;
+  if (vec) ha.h += (size_t)vec_row * o.d;
   ha.w = c->W<uint8_t>(o.head);
   ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
   ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
@@ -524,9 +534,9 @@ int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_b
   for (int i = i0; i <= k; ++i) {
     TokenSrc tok{nullptr, dk + (i - 1)};
     const int begin = i == 1 ? pass1_begin : 0;
-    int rc = run_layers(c, 1, true, tok, i - 1, begin, l, i == 1 ? qnet_after : 0, dk + i, s);
+    int rc = run_layers(c, 1, true, tok, i - 1, begin, l, i == 1 ? qnet_after : 0, dk + i, s, i - 1);
     if (rc) return rc;
-    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1, sampled), s);
+    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1, sampled), s, i - 1);
     if (rc) return rc;
     if (sampled) {
       SampleArgs sa{};
@@ -551,14 +561,30 @@ int push_trace(lede_ctx* c, const float* logits, int rows, const int32_t* record
   return LEDE_OK;
 }
 
-int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f) {
+// The pass of draft input k (the last draft) through layers [0, l) without a
+// head: with it, rows 0..k of the h buffer hold every verify row's hidden
+// state at layer l and the KV of positions c..c+k is written below l.
+int extend_drafts(lede_ctx* c, int l, int k, hipStream_t s) {
+  uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
+  return run_layers(c, 1, true, TokenSrc{nullptr, dk + k}, k, 0, l, 0, nullptr, s, k);
+}
+
+// The verify pass of rows [pending, d_1..d_k]: all layers from the embedding
+// (from_layer = 0), or layers [from_layer, L) on the hidden states the draft
+// passes left in rows 0..k (verify reuse), then the head and acceptance.
+int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from_layer = 0) {
   uint64_t* dk = c->S<uint64_t>(c->lo.dkeys);
   uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
   const bool sampled = inv_t > 0.f;
   const bool trace = c->lo.He > 0;
   TokenSrc tok{nullptr, dk};
-  int rc = run_layers(c, k + 1, false, tok, 0, 0, c->lo.L, 0, vk, s);
-  if (rc) return rc;
+  int rc;
+  if (from_layer >= c->lo.L) {
+    // no layer left: the head's argmax slots are cleared here
+    HIP_CHECK(c, launch_fill_u64(vk, 0, k + 1, s));
+  } else if ((rc = run_layers(c, k + 1, false, tok, 0, from_layer, c->lo.L, 0, vk, s))) {
+    return rc;
+  }
   rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s);
   if (rc) return rc;
   AcceptArgs aa{};
@@ -769,6 +795,13 @@ int lede_set_options(lede_ctx* c, int32_t use_graphs, int32_t debug) {
   return LEDE_OK;
 }
 
+int lede_set_verify_reuse(lede_ctx* c, int32_t enable) {
+  if (!c) return LEDE_E_ARG;
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  c->verify_reuse = enable != 0;
+  return LEDE_OK;
+}
+
 int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token) {
   if (!c || !tokens || n < 1) return fail(c, LEDE_E_ARG, "bad prefill arguments");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
@@ -880,7 +913,9 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
     if (rc) return rc;
     if ((rc = upload_table(c, s))) return rc;
   }
-  int rc = launch_verify(c, k, s);
+  const int from = (c->verify_reuse && k > 0) ? c->drafted_l : 0;
+  int rc = from ? extend_drafts(c, from, k, s) : LEDE_OK;
+  if (!rc) rc = launch_verify(c, k, s, 0.f, from);
   if (rc) return rc;
   if (verify) HIP_CHECK(c, hipMemcpyAsync(c->keys_h + 16, c->S<uint64_t>(c->lo.vkeys), 16 * 8, hipMemcpyDeviceToHost, s));
   rc = read_record(c, s);
@@ -961,7 +996,7 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
       const int qa = (want_q && l_min <= l) ? l_min : 0;
       ran_q = qa > 0;
-      if (c->use_graphs && !c->prof && s && !sampled) {
+      if (c->use_graphs && !c->prof && s && !sampled && !c->verify_reuse) {
         // the whole step as one graph: every launch reads positions, tokens
         // and pages from device memory, so a capture serves every step of
         // the same shape
@@ -980,10 +1015,12 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
     }
   }
   {
+    const int from = (c->verify_reuse && k_eff > 0) ? l : 0;
+    if (from && (rc = extend_drafts(c, l, k_eff, s))) return rc;
     if (k_eff > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
     hipEvent_t ph1 = nullptr;
     if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
-    rc = launch_verify(c, k_eff, s, inv_t);
+    rc = launch_verify(c, k_eff, s, inv_t, from);
     if (rc) return rc;
     if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
   }
@@ -1069,6 +1106,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
     return LEDE_OK;
   };
   int l_star = c->cfg.exits[c->cfg.n_exits - 1], k = 0;
+  bool ran_last = false;  // the pass of draft input k (the last draft) has run
   if (k_lim > 0) {
     // exit layer: up the candidate layers with the pending token (draft pass 1)
     int begin = 0;
@@ -1088,17 +1126,20 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
     k = 1;
     // draft length: each further pass at l* continues on 'exit'
     while (k < k_lim) {
-      rc = run_layers(c, 1, true, TokenSrc{nullptr, dk + k}, k, 0, l_star, 0, dk + k + 1, s);
-      if (!rc) rc = run_head(c, 1, true, dk + k + 1, draft_logits(c, k, true), s);
+      rc = run_layers(c, 1, true, TokenSrc{nullptr, dk + k}, k, 0, l_star, 0, dk + k + 1, s, k);
+      if (!rc) rc = run_head(c, 1, true, dk + k + 1, draft_logits(c, k, true), s, k);
       int act = 0;
       if (!rc) rc = decide(draft_logits(c, k, true), 1, k + 1, &act);
       if (rc) { truncate_pages(c, c0); return rc; }
+      ran_last = act != 1;  // 'continue': this pass was the last draft's input pass
       if (act != 1) break;
       ++k;
     }
     c->last_draft_rows = k;
   }
-  if ((rc = launch_verify(c, k, s))) return rc;
+  const int from = (c->verify_reuse && k > 0) ? l_star : 0;
+  if (from && !ran_last && (rc = extend_drafts(c, l_star, k, s))) return rc;
+  if ((rc = launch_verify(c, k, s, 0.f, from))) return rc;
   if ((rc = read_record(c, s))) return rc;
   commit_host(c);
   if ((rc = prof_fold(c))) return rc;

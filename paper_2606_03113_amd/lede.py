@@ -66,7 +66,7 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
             "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
             "lede_op_read_probe", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
-            "lede_get_trace", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
+            "lede_get_trace", "lede_set_verify_reuse", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
             "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
             "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read"]
 SAMPLE_SLOTS = 16
@@ -94,6 +94,7 @@ def load(path: str = LIB_PATH):
     L.lede_load_tensor.argtypes = [vp, i32, i32, vp, vp]
     L.lede_set_free_list.argtypes = [vp, P(i32), i32]
     L.lede_set_options.argtypes = [vp, i32, i32]
+    L.lede_set_verify_reuse.argtypes = [vp, i32]
     L.lede_prefill.argtypes = [vp, P(i32), i32, vp, P(i32)]
     L.lede_set_pending.argtypes = [vp, i32, vp]
     L.lede_truncate.argtypes = [vp, i32, vp]
@@ -265,6 +266,9 @@ class Engine:
     # -- C-ABI calls (same names) --------------------------------------------------
     def lede_set_options(self, use_graphs: int = 0, debug: int = 0):
         self._check(self.L.lede_set_options(self.ctx, use_graphs, debug), self.ctx)
+
+    def lede_set_verify_reuse(self, enable: bool = True):
+        self._check(self.L.lede_set_verify_reuse(self.ctx, int(enable)), self.ctx)
 
     def lede_set_free_list(self, order: Sequence[int]):
         a = np.ascontiguousarray(order, dtype=np.int32)

@@ -3,7 +3,7 @@ configuration bench.py times (512-token prompt, exit layer 8, draft length
 4, Q-network logged): the prefill's last-row logits and the first
 self-speculative steps (every draft row, every verify row up to the
 acceptance point, the Q-values, acceptance, KV length and page table)
-against the fp64 oracle; and, as a property that holds at any size, greedy
+against the fp64 oracle, then two steps with verify reuse; and, as a property that holds at any size, greedy
 self-speculative output equal to greedy autoregressive output on the GPU."""
 import time
 
@@ -66,6 +66,13 @@ def test_fullsize_prefill_and_ssd_steps_match_oracle(inputs):
     say("  ssd steps=%d rows=%d max_err/tol=%.3g max_abs=%.3g substitutions=%d" %
         (rep.steps, rep.rows, rep.max_err_rel, rep.max_err_abs, rep.substitutions))
     assert rep.steps >= 3
+    # two more steps with the verify starting at the exit layer
+    eng.lede_set_verify_reuse(True)
+    n0 = rep.steps
+    check_ssd(eng, st, m, len(st.out) + 2 * (k + 1), [(l, k)], rep, qnet_log=True)
+    say("  verify-reuse steps=%d max_err/tol=%.3g substitutions=%d" %
+        (rep.steps - n0, rep.max_err_rel, rep.substitutions))
+    assert rep.steps >= n0 + 2
 
 
 def test_fullsize_ssd_equals_ar_on_gpu(inputs):
