@@ -168,6 +168,8 @@ def main():
     ap.add_argument("--prof-steps", type=int, default=30)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dqn", action="store_true", help="skip the policy-trainer update timing")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time the exit layer x draft length grid {4,8,12,16} x {2,4,6,8} (llama2-7b)")
     ap.add_argument("--verify-reuse", action="store_true",
                     help="verify from the exit layer on the draft passes' hidden states and KV")
     ap.add_argument("--graphs", type=int, default=0)
@@ -312,6 +314,46 @@ def main():
     ar_ms = e0.elapsed_time(e1)
     ar_bytes = sum(verify_bytes(m, 0, r.seq_len - 1) for r in ar_recs)
 
+    sweep = None
+    if args.sweep:
+        # the workload's (exit layer x draft length) grid from the prompt state:
+        # 20 timed steps per point, then 10 with the draft / verify phases timed
+        sweep = []
+        for ls in (4, 8, 12, 16):
+            for ks in (2, 4, 6, 8):
+                gen = [1]
+
+                def fixed_step():
+                    r = eng.lede_step((ls, ks), n_remaining=max(1, wl.n_gen - gen[0]), log_qnet=log_q)
+                    gen[0] += len(r.emitted)
+                    return r
+                eng.lede_truncate(wl.prompt_len)
+                eng.lede_set_pending(first)
+                for _ in range(2):
+                    fixed_step()
+                torch.cuda.synchronize()
+                e0.record(stream)
+                rs = [fixed_step() for _ in range(20)]
+                e1.record(stream)
+                torch.cuda.synchronize()
+                sw_ms = e0.elapsed_time(e1)
+                eng.lede_prof_enable(1)
+                eng.lede_prof_read(reset=True)
+                prs = [fixed_step() for _ in range(10)]
+                pr = eng.lede_prof_read(reset=True)
+                eng.lede_prof_enable(0)
+                sdb = svb = 0.0
+                for r in prs:
+                    c = r.seq_len - r.accepted - 1
+                    sdb += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff)) + (m.qnet_bytes() if log_q else 0)
+                    svb += verify_bytes(m, r.k_eff, c)
+                dpm, vpm = pr["draft_phase"]["ms"], pr["verify_phase"]["ms"]
+                sweep.append({"l": ls, "k": ks, "ms_per_step": round(sw_ms / 20, 4),
+                              "tokens_per_s": round(sum(len(r.emitted) for r in rs) / (sw_ms / 1e3), 2),
+                              "draft_frac": round(sdb / (dpm * 1e6) / HBM_PEAK_GBPS, 4) if dpm else None,
+                              "verify_frac": round(svb / (vpm * 1e6) / HBM_PEAK_GBPS, 4) if vpm else None})
+                log("sweep l=%d k=%d: %.3f ms/step" % (ls, ks, sw_ms / 20))
+
     # achievable read bandwidth: the weight arena read once by the probe kernel
     from paper_2606_03113_amd import op_read_probe
     probe_bytes = eng.weights.numel() // 16 * 16
@@ -393,6 +435,8 @@ def main():
                            "frac": round(max(probe.values()) / HBM_PEAK_GBPS, 4),
                            "bytes": probe_bytes, "by_grid": {str(g): round(v, 1) for g, v in probe.items()}},
     }
+    if sweep is not None:
+        out["sweep"] = sweep
     if not args.no_dqn:
         log("policy trainer updates ...")
         out["dqn"] = dqn_leg(torch, li)
