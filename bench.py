@@ -361,6 +361,32 @@ def main():
     for grid in (1024, 4096, 16384):
         op_read_probe(eng.weights[:probe_bytes], grid)
         probe[grid] = probe_bytes / (min(op_read_probe(eng.weights[:probe_bytes], grid) for _ in range(3)) * 1e6)
+    # the same read with the one-row linear kernel's load structure and no
+    # arithmetic, per matrix shape of a draft pass, from arena regions not read
+    # for at least 600 MB (beyond the 256 MB memory-side cache)
+    from paper_2606_03113_amd import op_read_groups
+    kt = lambda K: -(-K // (32 if m.dtype == "bf16" else 16))  # noqa: E731
+    qkv_rows = m.n_heads * m.head_dim + 2 * m.n_kv_heads * m.head_dim
+    shapes = {"qkv": (qkv_rows // 16, kt(m.d_model)), "o": (m.d_model // 16, kt(m.n_heads * m.head_dim)),
+              "gate_up": (2 * m.ffn_dim // 16, kt(m.d_model)), "down": (m.d_model // 16, kt(m.ffn_dim)),
+              "head": (m.vocab // 16, kt(m.d_model))}
+    arena = eng.weights.numel()
+    ceiling = {}
+    rot = 0
+    for name, (ng, nt) in shapes.items():
+        size = ng * nt * 1024
+        ts = []
+        for _ in range(4):
+            off = (rot * (600 << 20)) % (arena - size) // 256 * 256
+            rot += 1
+            ts.append(op_read_groups(eng.weights[off:off + size], ng, nt))
+        t = min(ts[1:])
+        ceiling[name] = {"groups": ng, "MB": round(size / 1e6, 1), "us": round(1e3 * t, 2),
+                         "GBps": round(size / (t * 1e6), 1)}
+    # one draft pass at the workload's exit layer, weights only
+    pass_w = l * sum(ceiling[n]["MB"] for n in ("qkv", "o", "gate_up", "down")) + ceiling["head"]["MB"]
+    pass_t = l * sum(ceiling[n]["us"] for n in ("qkv", "o", "gate_up", "down")) + ceiling["head"]["us"]
+    vec_ceiling = 1e3 * pass_w / pass_t  # GB/s
     from paper_2606_03113_amd.lede import K_SYMBOLS
     lin = {n: prof[n] for n in K_SYMBOLS}
     # the linear class that moves the most algorithmic bytes per step (a choice by
@@ -431,6 +457,8 @@ def main():
         "ar": {"tokens_per_s": round(n_ar / (ar_ms / 1e3), 3), "ms_per_token": round(ar_ms / n_ar, 4),
                "GBps": round(ar_bytes / (ar_ms * 1e6), 1), "frac": round(ar_bytes / (ar_ms * 1e6) / HBM_PEAK_GBPS, 4),
                "ssd_speedup": round((acc_tokens / (ms / 1e3)) / (n_ar / (ar_ms / 1e3)), 4)},
+        "load_structure_ceiling": {"shapes": ceiling, "draft_pass_GBps": round(vec_ceiling, 1),
+                                   "roofline_kernel_vs_ceiling": round(achieved / vec_ceiling, 4)},
         "hbm_read_probe": {"GBps": round(max(probe.values()), 1),
                            "frac": round(max(probe.values()) / HBM_PEAK_GBPS, 4),
                            "bytes": probe_bytes, "by_grid": {str(g): round(v, 1) for g, v in probe.items()}},

@@ -421,6 +421,17 @@ int lede_op_sample(const float* logits, int32_t V, float temperature, float u, i
 int lede_op_read_probe(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream,
                        float* kernel_ms);
 
+/* The one-row linear kernel's memory access alone: reads n_groups (1..65535)
+ * groups of `tiles` (>= 1) contiguous 1 KiB weight tiles from the device
+ * buffer src (n_groups * tiles KiB) with that kernel's load structure, one
+ * group per block of 8 wavefronts, 4 non-temporal 16-byte loads per lane in
+ * flight; one uint32 per block goes to the device buffer sink [n_groups].
+ * The per-launch read rate of a matrix shape without any arithmetic, to set
+ * the kernel's times against.  kernel_ms as for lede_op_read_probe.
+ * LEDE_E_ARG on bad arguments, LEDE_E_HIP on a HIP error. */
+int lede_op_read_groups(const void* src, int32_t n_groups, int32_t tiles, uint32_t* sink, void* stream,
+                        float* kernel_ms);
+
 #ifdef __cplusplus
 }
 #endif

@@ -143,6 +143,10 @@ hipError_t launch_fill_u64(uint64_t* p, uint64_t v, int n, hipStream_t s);
 // the kernel's execution.
 hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int grid, hipStream_t s,
                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
+// Reads n_groups groups of `tiles` weight tiles (contiguous) with the one-row
+// linear kernel's load structure, one group per block.
+hipError_t launch_read_groups(const void* src, int n_groups, int tiles, uint32_t* sink, hipStream_t s,
+                              hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 hipError_t launch_set_token(uint64_t* keys, int idx, int token, hipStream_t s);
 hipError_t launch_dqn_init(const DqnInitArgs& a, hipStream_t s);
 hipError_t launch_dqn_update(const DqnUpdateArgs& a, hipStream_t s);

@@ -68,6 +68,36 @@ __global__ __launch_bounds__(256) void k_read_probe(const uint8_t* src, size_t n
   if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
 }
 
+// Reads n_groups x tiles tiles of TILE_BYTES with the one-row linear kernel's
+// load structure and nothing else: one group per block, LIN_WAVES wavefronts
+// splitting the group's tiles, LIN_TILES_PER_WAVE non-temporal 16-byte loads
+// per lane in flight per batch.  The XOR of the data goes to sink[block].
+__global__ __launch_bounds__(LIN_WAVES * 64) void k_read_groups(const uint8_t* src, int tiles, uint32_t* sink) {
+  constexpr int NW = LIN_WAVES, U = LIN_TILES_PER_WAVE;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint8_t* base = src + (size_t)blockIdx.x * tiles * TILE_BYTES + lane * 16;
+  uint32_t acc = 0;
+  for (int t0 = wave; t0 < tiles; t0 += NW * U) {
+    uint4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int t = t0 + NW * u;
+      v[u] = t < tiles ? ld16_stream(base + (size_t)t * TILE_BYTES) : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  __shared__ uint32_t red[NW];
+  for (int o = 32; o > 0; o >>= 1) acc ^= __shfl_xor(acc, o);
+  if (lane == 0) red[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t x = 0;
+    for (int w = 0; w < NW; ++w) x ^= red[w];
+    sink[blockIdx.x] = x;
+  }
+}
+
 // ---- launchers ----------------------------------------------------------------
 
 hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s) {
@@ -82,6 +112,16 @@ hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, int 
                           sink);
   else
     hipLaunchKernelGGL(k_read_probe, dim3(grid), dim3(256), 0, s, (const uint8_t*)src, bytes / 16, sink);
+  return hipGetLastError();
+}
+
+hipError_t launch_read_groups(const void* src, int n_groups, int tiles, uint32_t* sink, hipStream_t s,
+                              hipEvent_t e0, hipEvent_t e1) {
+  if (e0)
+    hipExtLaunchKernelGGL(k_read_groups, dim3(n_groups), dim3(LIN_WAVES * 64), 0, s, e0, e1, 0, (const uint8_t*)src,
+                          tiles, sink);
+  else
+    hipLaunchKernelGGL(k_read_groups, dim3(n_groups), dim3(LIN_WAVES * 64), 0, s, (const uint8_t*)src, tiles, sink);
   return hipGetLastError();
 }
 

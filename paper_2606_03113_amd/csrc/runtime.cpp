@@ -1320,6 +1320,23 @@ int lede_op_read_probe(const void* src, size_t bytes, uint32_t* sink, int32_t gr
   return rc;
 }
 
+int lede_op_read_groups(const void* src, int32_t n_groups, int32_t tiles, uint32_t* sink, void* stream,
+                        float* kernel_ms) {
+  if (!src || !sink || n_groups < 1 || n_groups > 65535 || tiles < 1) return LEDE_E_ARG;
+  if (!kernel_ms)
+    return launch_read_groups(src, n_groups, tiles, sink, S_(stream)) == hipSuccess ? LEDE_OK : LEDE_E_HIP;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess) return LEDE_E_HIP;
+  if (hipEventCreate(&e1) != hipSuccess) { (void)hipEventDestroy(e0); return LEDE_E_HIP; }
+  int rc = LEDE_OK;
+  if (launch_read_groups(src, n_groups, tiles, sink, S_(stream), e0, e1) != hipSuccess ||
+      hipEventSynchronize(e1) != hipSuccess || hipEventElapsedTime(kernel_ms, e0, e1) != hipSuccess)
+    rc = LEDE_E_HIP;
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return rc;
+}
+
 }  // extern "C"
 
 // ---- views for the policy trainer (dqn.cpp) ----------------------------------------

@@ -65,7 +65,7 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_set_free_list", "lede_set_options", "lede_prefill", "lede_set_pending", "lede_truncate",
             "lede_draft", "lede_verify", "lede_step", "lede_get_kv_state", "lede_debug_read",
             "lede_prof_enable", "lede_prof_read", "lede_op_tiled_bytes", "lede_op_repack", "lede_op_linear",
-            "lede_op_read_probe", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
+            "lede_op_read_probe", "lede_op_read_groups", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
             "lede_get_trace", "lede_set_verify_reuse", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
             "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
             "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read"]
@@ -110,6 +110,7 @@ def load(path: str = LIB_PATH):
     L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
     L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, vp, i32, vp]
     L.lede_op_read_probe.argtypes = [vp, sz, vp, i32, vp, P(ctypes.c_float)]
+    L.lede_op_read_groups.argtypes = [vp, i32, i32, vp, vp, P(ctypes.c_float)]
     L.lede_step_sampled.argtypes = [vp, P(LedeAction), i32, i32, ctypes.c_float, P(ctypes.c_float), vp,
                                     P(LedeStepRecord)]
     L.lede_op_sample.argtypes = [vp, i32, ctypes.c_float, ctypes.c_float, P(i32), vp]
@@ -426,6 +427,22 @@ def op_read_probe(buf, grid: int = 0) -> float:
     rc = L.lede_op_read_probe(buf.data_ptr(), nbytes, sink.data_ptr(), int(grid), s, ctypes.byref(ms))
     if rc:
         raise LedeError(rc, "op_read_probe")
+    return ms.value
+
+
+def op_read_groups(buf, n_groups: int, tiles: int) -> float:
+    """Kernel milliseconds for reading n_groups x tiles 1 KiB tiles at the start
+    of the GPU tensor buf with the one-row linear kernel's load structure."""
+    import torch
+    L = load()
+    if n_groups * tiles * 1024 > buf.numel() * buf.element_size():
+        raise LedeError(LEDE_E_ARG, "buffer smaller than n_groups x tiles KiB")
+    sink = torch.empty(n_groups, dtype=torch.int32, device=buf.device)
+    ms = ctypes.c_float()
+    s = ctypes.c_void_p(torch.cuda.current_stream(buf.device).cuda_stream)
+    rc = L.lede_op_read_groups(buf.data_ptr(), int(n_groups), int(tiles), sink.data_ptr(), s, ctypes.byref(ms))
+    if rc:
+        raise LedeError(rc, "op_read_groups")
     return ms.value
 
 

@@ -90,6 +90,11 @@ def test_read_probe_rejects_bad_arguments(lib):
     assert lib.lede_op_read_probe(src, 1024, sink, 0, None, None) == lede.LEDE_E_ARG
     assert lib.lede_op_read_probe(src, 1024, sink, 65536, None, None) == lede.LEDE_E_ARG
     assert lib.lede_op_read_probe(src, 1024, None, 4, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_groups(None, 4, 8, sink, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_groups(src, 0, 8, sink, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_groups(src, 65536, 8, sink, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_groups(src, 4, 0, sink, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_op_read_groups(src, 4, 8, None, None, None) == lede.LEDE_E_ARG
 
 
 def test_sampling_entry_points_reject_bad_arguments(lib):

@@ -98,3 +98,21 @@ def test_read_probe_reads_every_word(n_words, grid):
     got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     assert got == np.bitwise_xor.reduce(words)
     assert op_read_probe(buf) > 0
+
+
+@pytest.mark.parametrize("n_groups,tiles", [(1, 1), (3, 37), (256, 128), (17, 344)])
+def test_read_groups_reads_every_word(n_groups, tiles):
+    """The group-structured read probe touches every word of its groups once
+    (ragged batches included): the XOR of its per-block results equals the
+    XOR of all words, and nothing past the groups is read into it."""
+    from paper_2606_03113_amd import op_read_groups, load
+    import ctypes
+    n_words = n_groups * tiles * 256
+    words = li.uniform_int(5, 10, n_words + 256, 0, (1 << 31) - 1).view(np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).to("cuda")
+    sink = torch.zeros(n_groups, dtype=torch.int32, device="cuda")
+    s = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert load().lede_op_read_groups(buf.data_ptr(), n_groups, tiles, sink.data_ptr(), s, None) == 0
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(words[:n_words])
+    assert op_read_groups(buf, n_groups, tiles) > 0
