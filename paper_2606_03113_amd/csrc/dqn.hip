@@ -62,6 +62,24 @@ __global__ __launch_bounds__(DQN_THREADS) void k_dqn_update(DqnUpdateArgs a) {
   __shared__ int act[DQN_MAX_BATCH], boot[DQN_MAX_BATCH];
   const int tid = threadIdx.x, NT = DQN_THREADS;
   const int H = a.H, B = a.B, P = dqn_params(H), NC = dqn_noise(H);
+  // parameter p = tid + NT i of a set: its mean and scale, their Adam
+  // moments and the target's, all requested up front (one round trip)
+  constexpr int PI = (6 * DQN_MAX_HIDDEN + 2 + DQN_THREADS - 1) / DQN_THREADS;
+  float th_mu[PI], th_sg[PI], m_mu[PI], m_sg[PI], v_mu[PI], v_sg[PI], tg_mu[PI], tg_sg[PI];
+#pragma unroll
+  for (int i = 0; i < PI; ++i) {
+    const int p = tid + NT * i;
+    if (p < P) {
+      th_mu[i] = a.theta[p];
+      th_sg[i] = a.theta[P + p];
+      tg_mu[i] = a.target[p];
+      tg_sg[i] = a.target[P + p];
+      m_mu[i] = a.m[p];
+      m_sg[i] = a.m[P + p];
+      v_mu[i] = a.v[p];
+      v_sg[i] = a.v[P + p];
+    }
+  }
 
   // noise of both networks, then their weights for this draw
   for (int i = tid; i < NC; i += NT) {
@@ -69,9 +87,13 @@ __global__ __launch_bounds__(DQN_THREADS) void k_dqn_update(DqnUpdateArgs a) {
     nf_tg[i] = noise_f(a.noise[NC + i]);
   }
   __syncthreads();
-  for (int p = tid; p < P; p += NT) {
-    w_on[p] = a.theta[p] + a.theta[P + p] * noise_of(nf_on, H, p);
-    w_tg[p] = a.target[p] + a.target[P + p] * noise_of(nf_tg, H, p);
+#pragma unroll
+  for (int i = 0; i < PI; ++i) {
+    const int p = tid + NT * i;
+    if (p < P) {
+      w_on[p] = th_mu[i] + th_sg[i] * noise_of(nf_on, H, p);
+      w_tg[p] = tg_mu[i] + tg_sg[i] * noise_of(nf_tg, H, p);
+    }
   }
   // sampled transitions: position floor(m * n_valid / 2^24) of the stored
   // ones (oldest first), the discounted sum of up to n rewards (stopping
@@ -85,15 +107,20 @@ __global__ __launch_bounds__(DQN_THREADS) void k_dqn_update(DqnUpdateArgs a) {
     sx[b][1] = s0[1];
     sx[b][2] = s0[2];
     act[b] = s0[3] > 0.5f ? 1 : 0;
+    // every reward and terminal flag of the window is requested before the
+    // first is used (one round trip), then folded in order
+    float2 rd[DQN_MAX_N];
+#pragma unroll
+    for (int k = 0; k < DQN_MAX_N; ++k)
+      if (k < a.n) rd[k] = *(const float2*)(a.ring + (size_t)((a.oldest + j + k) % a.capacity) * DQN_SLOT + 4);
     float R = 0.f, gk = 1.f;
     int bt = 1;
-    for (int k = 0; k < a.n; ++k) {
-      const float* sl = a.ring + (size_t)((a.oldest + j + k) % a.capacity) * DQN_SLOT;
-      R += gk * sl[4];
-      gk *= a.gamma;
-      if (sl[5] != 0.f) {
-        bt = 0;
-        break;
+#pragma unroll
+    for (int k = 0; k < DQN_MAX_N; ++k) {
+      if (k < a.n && bt) {
+        R += gk * rd[k].x;
+        gk *= a.gamma;
+        if (rd[k].y != 0.f) bt = 0;
       }
     }
     ret[b] = R;
@@ -168,14 +195,23 @@ __global__ __launch_bounds__(DQN_THREADS) void k_dqn_update(DqnUpdateArgs a) {
   }
   __syncthreads();
   // Adam: d/dmu = g, d/dsigma = g * noise
-  for (int p = tid; p < 2 * P; p += NT) {
-    const float g = p < P ? grad[p] : grad[p - P] * noise_of(nf_on, H, p - P);
-    const float m = a.beta1 * a.m[p] + (1.f - a.beta1) * g;
-    const float v = a.beta2 * a.v[p] + (1.f - a.beta2) * g * g;
-    a.m[p] = m;
-    a.v[p] = v;
+  auto adam = [&](float g, float& th, float& m, float& v, size_t q) {
+    m = a.beta1 * m + (1.f - a.beta1) * g;
+    v = a.beta2 * v + (1.f - a.beta2) * g * g;
+    a.m[q] = m;
+    a.v[q] = v;
     const float mh = m / a.bc1, vh = v / a.bc2;
-    a.theta[p] -= a.lr * (mh / (sqrtf(vh) + a.eps));
+    th -= a.lr * (mh / (sqrtf(vh) + a.eps));
+    a.theta[q] = th;
+  };
+#pragma unroll
+  for (int i = 0; i < PI; ++i) {
+    const int p = tid + NT * i;
+    if (p < P) {
+      const float g = grad[p];
+      adam(g, th_mu[i], m_mu[i], v_mu[i], p);
+      adam(g * noise_of(nf_on, H, p), th_sg[i], m_sg[i], v_sg[i], (size_t)P + p);
+    }
   }
 }
 
