@@ -179,6 +179,171 @@ __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
   Elem<DT>::store(a.out, (size_t)m * a.ldo + head * HD + i, acc / l);
 }
 
+// Eight fp32 values as bf16 high parts and the bf16 rounding of what is left,
+// packed as two matrix-core fragments: x ~= hi + lo to about 16 bits.
+__device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint16_t h0 = f32_to_bf16(x[2 * i]), h1 = f32_to_bf16(x[2 * i + 1]);
+    const uint16_t l0 = f32_to_bf16(x[2 * i] - bf16_to_f32(h0)), l1 = f32_to_bf16(x[2 * i + 1] - bf16_to_f32(h1));
+    h[i] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+    l[i] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+  }
+  hi = make_uint4(h[0], h[1], h[2], h[3]);
+  lo = make_uint4(l[0], l[1], l[2], l[3]);
+}
+
+// Partial attention on the matrix cores (bf16 cache), the same partials as
+// k_attn_partial for up to 16 query rows per block: per page, wavefront w
+// scores the page's tokens 16w..16w+15 against all rows (S^T = K Q^T as
+// 16x16x32 tiles, q split into bf16 high and low parts), the page's per-row
+// max and sum combine the four wavefronts in order through LDS, and
+// wavefront w forms its HD/4 output dims as V^T P^T (the weights split the
+// same way; the wavefront's value columns are staged in LDS and read back
+// transposed).  Every output element is a fixed-order function of its own
+// row, so a row's partials do not depend on the rows sharing its block.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
+  constexpr int KS = HD / 32;          // k-steps of the scores
+  constexpr int DW = HD / 4;           // output dims per wavefront
+  constexpr int DT = DW / 16;          // 16-dim output tiles per wavefront
+  constexpr int VS = DW + 4;           // LDS row stride (elements) of the staged values
+  __shared__ float smax[4][16], ssum[4][16];
+  __shared__ float ps[16][64 + 4];
+  __shared__ uint16_t vs[4][64 * VS];
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, lr = l & 15, lg = l >> 4;
+  const int G = a.nq / a.nkv;
+  const int R = a.M * G;
+  const int n_rs = (R + a.rows_per_block - 1) / a.rows_per_block;
+  const int kvh = blockIdx.x / n_rs, rs = blockIdx.x % n_rs;
+  const int r0 = rs * a.rows_per_block;
+  const int nr = min(a.rows_per_block, R - r0);
+  const int pos0 = *a.seq_len + a.pos_off;
+  const int pmax = pos0 + a.M - 1;
+  const int n_chunks = pmax / 64 + 1;
+  if ((int)blockIdx.y >= n_chunks) return;
+  // this lane's query row as a matrix-core operand (rows past nr are zero)
+  const bool row_ok = lr < nr;
+  const int rr = r0 + lr, m_row = row_ok ? rr / G : 0, head = kvh * G + (row_ok ? rr % G : 0);
+  const int row_pos = pos0 + m_row;
+  uint4 qh[KS], ql[KS];
+  {
+    const float scale = rsqrtf((float)HD);
+    const float* qp = a.q + (size_t)m_row * a.ldq + head * HD + lg * 8;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      float x[8];
+      if (row_ok) {
+        const float4 u = *(const float4*)(qp + 32 * s2), v = *(const float4*)(qp + 32 * s2 + 4);
+        x[0] = u.x * scale; x[1] = u.y * scale; x[2] = u.z * scale; x[3] = u.w * scale;
+        x[4] = v.x * scale; x[5] = v.y * scale; x[6] = v.z * scale; x[7] = v.w * scale;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = 0.f;
+      }
+      split8(x, qh[s2], ql[s2]);
+    }
+  }
+  const uint16_t* kc = (const uint16_t*)a.kcache;
+  const uint16_t* vc = (const uint16_t*)a.vcache;
+  for (int j = blockIdx.y; j < n_chunks; j += a.n_split) {
+    const int page = a.block_table[j];
+    const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
+    const int nvalid = min(64, pmax - j * 64 + 1);
+    // keys of tokens 16w + lr, dims 32 s + 8 lg; values of this wavefront's dims
+    uint4 kf[KS];
+    const int tk = 16 * w + lr;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2)
+      kf[s2] = tk < nvalid ? ld16(kc + base + (size_t)tk * HD + 32 * s2 + 8 * lg) : make_uint4(0u, 0u, 0u, 0u);
+    constexpr int VC = 64 * DW / 8 / 64;   // 16-byte value chunks per lane
+    uint4 vf[VC];
+#pragma unroll
+    for (int c = 0; c < VC; ++c) {
+      const int idx = l + 64 * c, t = idx / (DW / 8), d8 = idx % (DW / 8);
+      vf[c] = t < nvalid ? ld16(vc + base + (size_t)t * HD + w * DW + 8 * d8) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    // S^T tile: lane holds tokens 16w + 4 lg + i of row lr
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      sc = mfma_tile<1>(kf[s2], qh[s2], sc);
+      sc = mfma_tile<1>(kf[s2], ql[s2], sc);
+    }
+    float sv[4], mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = j * 64 + 16 * w + 4 * lg + i;
+      sv[i] = (row_ok && t <= row_pos) ? sc[i] : -INFINITY;
+      mx = fmaxf(mx, sv[i]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (lg == 0) smax[w][lr] = mx;
+#pragma unroll
+    for (int c = 0; c < VC; ++c) {
+      const int idx = l + 64 * c, t = idx / (DW / 8), d8 = idx % (DW / 8);
+      uint16_t* dst = &vs[w][t * VS + 8 * d8];
+      *(uint2*)dst = make_uint2(vf[c].x, vf[c].y);
+      *(uint2*)(dst + 4) = make_uint2(vf[c].z, vf[c].w);
+    }
+    __syncthreads();
+    const float pm = fmaxf(fmaxf(fmaxf(smax[0][lr], smax[1][lr]), smax[2][lr]), smax[3][lr]);
+    float pv[4], sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pv[i] = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - pm);
+      sum += pv[i];
+    }
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    if (lg == 0) ssum[w][lr] = sum;
+    *(float4*)&ps[lr][16 * w + 4 * lg] = make_float4(pv[0], pv[1], pv[2], pv[3]);
+    __syncthreads();
+    // this wavefront's dims: D^T = V^T P^T over the page's 64 tokens
+    f32x4 oc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      float px[8];
+      const float4 u = *(const float4*)&ps[lr][32 * ks + 8 * lg], v = *(const float4*)&ps[lr][32 * ks + 8 * lg + 4];
+      px[0] = u.x; px[1] = u.y; px[2] = u.z; px[3] = u.w; px[4] = v.x; px[5] = v.y; px[6] = v.z; px[7] = v.w;
+      uint4 ph, pl;
+      split8(px, ph, pl);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d = 16 * dt + lr;
+        uint32_t e[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t = 32 * ks + 8 * lg + 2 * i;
+          e[i] = (uint32_t)vs[w][t * VS + d] | ((uint32_t)vs[w][(t + 1) * VS + d] << 16);
+        }
+        const uint4 vt = make_uint4(e[0], e[1], e[2], e[3]);
+        oc[dt] = mfma_tile<1>(vt, ph, oc[dt]);
+        oc[dt] = mfma_tile<1>(vt, pl, oc[dt]);
+      }
+    }
+    // partials of row lr: dims w * DW + 16 dt + 4 lg + i
+    if (row_ok) {
+      float* p = a.part + (((size_t)m_row * a.nq + head) * a.max_chunks + j) * (HD + 2);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d0 = w * DW + 16 * dt + 4 * lg;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[2 + d0 + i] = oc[dt][i];
+      }
+      if (w == 0 && lg == 0) {
+        p[0] = pm;
+        p[1] = ((ssum[0][lr] + ssum[1][lr]) + ssum[2][lr]) + ssum[3][lr];
+      }
+    }
+    __syncthreads();  // the next page rewrites the staging
+  }
+}
+
 hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   const int G = a.nq / a.nkv;
   const int n_rs = (a.M * G + a.rows_per_block - 1) / a.rows_per_block;
@@ -186,10 +351,12 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   const int combine_grid = a.M * a.nq;
   if (dtype == 1) {
     if (a.hd == 128) {
-      hipLaunchKernelGGL((k_attn_partial<1, 128>), grid, dim3(256), 0, s, a);
+      if (a.mfma) hipLaunchKernelGGL((k_attn_mfma<128>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_partial<1, 128>), grid, dim3(256), 0, s, a);
       hipLaunchKernelGGL((k_attn_combine<1, 128>), dim3(combine_grid), dim3(128), 0, s, a);
     } else {
-      hipLaunchKernelGGL((k_attn_partial<1, 64>), grid, dim3(256), 0, s, a);
+      if (a.mfma) hipLaunchKernelGGL((k_attn_mfma<64>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_partial<1, 64>), grid, dim3(256), 0, s, a);
       hipLaunchKernelGGL((k_attn_combine<1, 64>), dim3(combine_grid), dim3(64), 0, s, a);
     }
   } else {

@@ -31,6 +31,7 @@ struct AttnArgs {
   int max_chunks;
   float* part;                     // [M][nq][max_chunks][hd + 2]
   void* out; int ldo;              // combine output [M][nq*hd], model dtype
+  int mfma;                        // bf16: partials on the matrix cores (rows of verify, prefill, AR)
 };
 
 struct QnetOutArgs {

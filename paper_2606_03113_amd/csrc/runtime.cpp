@@ -428,6 +428,10 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     at.max_chunks = o.max_chunks;
     at.part = c->S<float>(o.part);
     at.out = c->S<void>(o.attn_out); at.ldo = o.qd;
+    // bf16 partials on the matrix cores for every multi-row pass (verify,
+    // autoregressive, prefill: one kernel whatever the row count, so a row's
+    // bits do not depend on it) and for one-row passes with grouped heads
+    at.mfma = dt == 1 && (!vec || G > 1);
     const double n_pos = (double)c->seq_len + pos_off + M;
     LAUNCH(LEDE_K_ATTENTION, n_pos * o.kvd * 2.0 * o.es + 2.0 * M * o.qd * 4,
            launch_attention(dt, at, s));

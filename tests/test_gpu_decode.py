@@ -219,3 +219,29 @@ def test_graph_replay_matches_eager(model):
             assert eager.lede_get_kv_state() == graphed.lede_get_kv_state()
             torch.ones(1024, device="cuda").sum().item()  # unrelated eager work on the same stream
         side.synchronize()
+
+
+@pytest.mark.parametrize("model", [TINY, SMALL_128], ids=lambda m: m.name)
+def test_longest_drafts_fill_the_verify_tile(model):
+    """k = 15, the most drafts one step takes: the verify pass carries 16 rows,
+    a full matrix-core tile, and the record holds 16 tokens."""
+    from paper_2606_03113_amd import Engine
+    say("k = 15", model.name)
+    eng = Engine(model, max_ctx=200, k_max=15)
+    w = li.weights(model)
+    q = li.qnet_weights(model)
+    eng.load_weights(w, q)
+    eng.lede_set_options(0, 1)
+    dec = make_decoder(model, w, q, 200)
+    st = SSDState(dec, 4, 64)
+    prompt = _prompt(model)
+    g = eng.lede_prefill(prompt)
+    st.prefill(prompt)
+    rep = Report()
+    if g != st.pending:
+        rep.token(model.dtype, g, dec.head(dec.forward(prompt, 0, model.n_layers)[-1:])[0])
+        eng.lede_set_pending(st.pending)
+    L = model.n_layers
+    check_ssd(eng, st, model, 1 + 60, [(1, 15), (L, 15), (2, 15)], rep)
+    say("  steps=%d rows=%d max_err/tol=%.3g subs=%d" % (rep.steps, rep.rows, rep.max_err_rel, rep.substitutions))
+    assert rep.steps >= 3
