@@ -394,7 +394,7 @@ def main():
     dom = max(lin, key=lambda n: lin[n]["bytes"])
     d = lin[dom]
     achieved = d["bytes"] / (d["ms"] * 1e6)  # GB/s
-    kname = K_SYMBOLS[dom]
+    kname = K_SYMBOLS[dom] if m.dtype == "bf16" else K_SYMBOLS[dom].replace("<1,", "<0,")
     traffic = traffic_from_profile(dom, wl.name, d["launches"])
     dp, vp = phases["draft_phase"], phases["verify_phase"]
     # algorithmic bytes of the phase-timed steps' passes

@@ -147,18 +147,20 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
-// Combine the per-page partials of every (row, head) in page order.
+// Combine the per-page partials of every (row, head) in page order (up to
+// 16 pages requested at once: one round trip for a 1024-token context).
 template <int DT, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
+  constexpr int B = 16;
   const int m = blockIdx.x / a.nq, head = blockIdx.x % a.nq, i = threadIdx.x;
   const int pos = *a.seq_len + a.pos_off + m;
   const int nc = pos / 64 + 1;
   const float* p = a.part + ((size_t)m * a.nq + head) * a.max_chunks * (HD + 2);
   float mx = -INFINITY, l = 0.f, acc = 0.f;
-  for (int j0 = 0; j0 < nc; j0 += 8) {
-    float pm[8], pl[8], pa[8];
+  for (int j0 = 0; j0 < nc; j0 += B) {
+    float pm[B], pl[B], pa[B];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < B; ++u) {
       const float* q = p + (size_t)(j0 + u) * (HD + 2);
       const bool ok = j0 + u < nc;
       pm[u] = ok ? q[0] : -INFINITY;
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
       pa[u] = ok ? q[2 + i] : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
+    for (int u = 0; u < B; ++u) {
       if (j0 + u >= nc) break;
       const float nm = fmaxf(mx, pm[u]);
       const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
