@@ -349,14 +349,10 @@ int linear_grid(int n_groups, int epi) {
   return epi == EPI_ARGMAX ? std::min(n_groups, 1024) : n_groups;
 }
 
-// The verify / prefill rows are normalised by the norm kernel (one
-// wavefront per row) rather than in every block of the matrix-core kernel:
-// re-reading k+1 residual rows per block costs more than one launch.
-bool fuse_norm(const lede_ctx* c, int M) {
-  (void)c;
-  (void)M;
-  return false;
-}
+// One-row passes normalise their input row in every block of the linear
+// kernel (the row is re-read from L2 by each block).  Multi-row passes use
+// the norm kernel, one block per row: re-reading k+1 residual rows in every
+// block of the matrix-core kernel costs more than the launch it saves.
 
 LinearArgs base_linear(const lede_ctx* c) {
   LinearArgs a{};
@@ -396,7 +392,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     qa.layer = j; qa.n_pages = o.n_pages; qa.nq = o.nq; qa.nkv = o.nkv; qa.hd = o.hd;
     qa.block_table = c->S<int32_t>(o.btab); qa.seq_len = c->S<int32_t>(o.seq_len); qa.pos_off = pos_off;
     qa.rope = c->S<float2>(o.rope);
-    if (vec || fuse_norm(c, M)) {
+    if (vec) {
       qa.x_mode = first ? X_EMBED_NORM : X_NORM;
       qa.gain = c->W<void>(lw.attn_norm);
       qa.embed = c->W<void>(o.embed);
@@ -452,7 +448,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     ga.w = c->W<uint8_t>(lw.wgu);
     ga.n_groups = 2 * o.F / 16; ga.KT = k_tiles(dt, o.d); ga.K = o.d;
     ga.epi = EPI_SWIGLU; ga.act = c->S<void>(o.act); ga.ld_act = o.Fp;
-    if (vec || fuse_norm(c, M)) {
+    if (vec) {
       ga.x_mode = X_NORM; ga.gain = c->W<void>(lw.ffn_norm);
     } else {
       NormArgs na{};
@@ -505,7 +501,7 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
   ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
   ha.logits = logits; ha.ld_logits = o.V;
-  if (vec || fuse_norm(c, M)) {
+  if (vec) {
     ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
   } else {
     NormArgs na{};
