@@ -22,7 +22,7 @@ __device__ void commit_step(const AcceptArgs& a, int acc, int y) {
   a.record[2] = c_new;
   a.record[3] = y;
   *a.seq_len = c_new;
-  a.pending_out[0] = (uint64_t)(0xFFFFFFFFu - (uint32_t)y);
+  key_store_token(a.pending_out, 0, y);
   const int keep = (c_new + 63) / 64, used = (c + k + 1 + 63) / 64;
   for (int j = keep; j < used; ++j) a.block_table[j] = -1;
 }
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(SB) void k_sample(SampleArgs a) {
   const int tok = block_draw([&](float x, float) { return expf((x - m) * it); }, a.logits, nullptr, a.vocab, u,
                              red, ired);
   if (threadIdx.x == 0) {
-    *a.key_out = (uint64_t)(0xFFFFFFFFu - (uint32_t)tok);
+    key_store_token(a.key_out, 0, tok);
     if (a.stats_out) {
       a.stats_out[0] = st.x;
       a.stats_out[1] = st.y;

@@ -52,13 +52,35 @@ enum XMode : int {
   X_F32 = 3,       // x fp32 [M][ldx] (the Q-network's fp32 layers)
 };
 
-// Token sources: int32 array, or 64-bit argmax keys (see ArgmaxKey).
+// Argmax keys.  Logical key i of a key buffer is spread over KEY_SLOTS words,
+// keys[s * KEY_PITCH + i] for s < KEY_SLOTS, 256 bytes apart: block b of a
+// head raises word b mod KEY_SLOTS with its atomic maximum, so that the
+// blocks of one launch contend on eight addresses instead of one, and the
+// key is the largest of its words.  A single writer stores word 0 and clears
+// the others.  A key buffer holds KEY_PITCH logical keys.
+constexpr int KEY_SLOTS = 8;
+constexpr int KEY_PITCH = 32;
+constexpr int KEY_WORDS = KEY_SLOTS * KEY_PITCH;
+
+__host__ __device__ inline uint64_t key_value(const uint64_t* keys, int i) {
+  uint64_t m = keys[i];
+  for (int s = 1; s < KEY_SLOTS; ++s) {
+    const uint64_t v = keys[s * KEY_PITCH + i];
+    m = v > m ? v : m;
+  }
+  return m;
+}
+__host__ __device__ inline int key_token(uint64_t key) { return (int)(0xFFFFFFFFu - (uint32_t)(key & 0xFFFFFFFFull)); }
+__host__ __device__ inline void key_store_token(uint64_t* keys, int i, int token) {
+  keys[i] = (uint64_t)(0xFFFFFFFFu - (uint32_t)token);
+  for (int s = 1; s < KEY_SLOTS; ++s) keys[s * KEY_PITCH + i] = 0;
+}
+
+// Token sources: int32 array, or argmax keys.
 struct TokenSrc {
   const int32_t* ids;   // if non-null
-  const uint64_t* keys; // else decode keys[i]
-  __host__ __device__ int get(int i) const {
-    return ids ? ids[i] : (int)(0xFFFFFFFFu - (uint32_t)(keys[i] & 0xFFFFFFFFull));
-  }
+  const uint64_t* keys; // else decode logical key i
+  __host__ __device__ int get(int i) const { return ids ? ids[i] : key_token(key_value(keys, i)); }
 };
 
 // Epilogues.
@@ -84,7 +106,7 @@ struct LinearArgs {
   float* h; int ldh;               // X_NORM / X_EMBED_NORM (and EPI_RESID target)
   const void* gain; float eps;
   const void* embed; TokenSrc tok;
-  uint64_t* zero_keys; int n_zero_keys;  // cleared by block 0 (argmax slots of a later head)
+  uint64_t* zero_keys; int n_zero_keys;  // logical keys cleared by block 0 (every slot; of a later head)
   // epilogue
   int epi;
   float* out; int ldo;             // EPI_STORE / EPI_BIAS_RELU

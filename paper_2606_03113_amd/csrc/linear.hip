@@ -250,7 +250,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   const int KT = a.KT, NG = a.n_groups;
   const uint4 zero = {0u, 0u, 0u, 0u};
 
-  if (blockIdx.x == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
+  if (blockIdx.x == 0 && a.zero_keys && tid < KEY_WORDS && (tid % KEY_PITCH) < a.n_zero_keys) a.zero_keys[tid] = 0;
 
   int g = blockIdx.x;
   // the weights do not depend on the input: the first batch is in flight
@@ -339,7 +339,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     __syncthreads();
   }
   if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
-    atomicMax((unsigned long long*)&a.keys[tid], (unsigned long long)best);
+    atomicMax((unsigned long long*)&a.keys[(blockIdx.x % KEY_SLOTS) * KEY_PITCH + tid], (unsigned long long)best);
 }
 
 // ---- launchers ----------------------------------------------------------------

@@ -39,7 +39,7 @@ __global__ void k_fill_u64(uint64_t* p, uint64_t v, int n) {
 }
 
 __global__ void k_set_token(uint64_t* keys, int idx, int token) {
-  if (threadIdx.x == 0) keys[idx] = (uint64_t)(0xFFFFFFFFu - (uint32_t)token);
+  if (threadIdx.x == 0) key_store_token(keys, idx, token);
 }
 
 // Achievable-bandwidth probe: every 16-byte chunk of src is read once with

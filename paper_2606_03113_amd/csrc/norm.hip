@@ -10,7 +10,7 @@ template <int DT>
 __global__ __launch_bounds__(256) void k_norm(NormArgs a) {
   __shared__ float scratch[4];
   const int m = blockIdx.x, tid = threadIdx.x;
-  if (m == 0 && a.zero_keys && tid < a.n_zero_keys) a.zero_keys[tid] = 0;
+  if (m == 0 && a.zero_keys && tid < KEY_WORDS && (tid % KEY_PITCH) < a.n_zero_keys) a.zero_keys[tid] = 0;
   float* h = a.h + (size_t)m * a.ldh;
   const float* src = h;
   const void* row = nullptr;

@@ -23,6 +23,7 @@ namespace {
 
 constexpr int PAGE = 64;
 constexpr int MROWS = 16;   // rows of one verify / prefill pass
+static_assert(MROWS <= KEY_PITCH && 15 + 2 <= KEY_PITCH, "a key buffer holds every row's key and every draft's");
 constexpr int RECORD_INTS = 64;
 constexpr int UNIF_FLOATS = 2 * SAMPLE_SLOTS + 1;  // uniforms of a sampled step
 
@@ -115,8 +116,8 @@ Layout make_layout(const lede_config* c) {
   o.act = take((size_t)MROWS * o.Fp * o.es);
   o.part = take((size_t)MROWS * o.nq * o.max_chunks * (o.hd + 2) * 4);
   o.logits = take((size_t)2 * MROWS * o.V * 4);
-  o.dkeys = take(32 * 8);
-  o.vkeys = take(MROWS * 8);
+  o.dkeys = take(KEY_WORDS * 8);
+  o.vkeys = take(KEY_WORDS * 8);
   o.qs = take((size_t)o.d * 4);
   o.qhid = take((size_t)(o.H ? o.H : 1) * 4);
   o.qv = take((size_t)(o.A ? o.A : 1) * 4);
@@ -581,7 +582,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from
   int rc;
   if (from_layer >= c->lo.L) {
     // no layer left: the head's argmax slots are cleared here
-    HIP_CHECK(c, launch_fill_u64(vk, 0, k + 1, s));
+    HIP_CHECK(c, launch_fill_u64(vk, 0, KEY_WORDS, s));
   } else if ((rc = run_layers(c, k + 1, false, tok, 0, from_layer, c->lo.L, 0, vk, s))) {
     return rc;
   }
@@ -690,7 +691,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
       hipHostMalloc((void**)&c->record_h, RECORD_INTS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->unif_h, UNIF_FLOATS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->trace_h, 64 * 4, 0) != hipSuccess ||
-      hipHostMalloc((void**)&c->keys_h, 32 * 8, 0) != hipSuccess) {
+      hipHostMalloc((void**)&c->keys_h, 2 * KEY_WORDS * 8, 0) != hipSuccess) {
     lede_destroy(c);
     return LEDE_E_HIP;
   }
@@ -834,9 +835,9 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
     last_m = M;
   }
   c->last_rows = last_m;
-  HIP_CHECK(c, hipMemcpyAsync(c->keys_h, vk, MROWS * 8, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipMemcpyAsync(c->keys_h, vk, KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
-  const int next = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[last_m - 1] & 0xFFFFFFFFull));
+  const int next = key_token(key_value(c->keys_h, last_m - 1));
   HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, next, s));
   rc = upload_seq_len(c, c0 + n, s);
   if (rc) return rc;
@@ -896,9 +897,9 @@ int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts)
   if (rc) return rc;
   c->policy_valid = 0;
   if (drafts) {
-    HIP_CHECK(c, hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), 32 * 8, hipMemcpyDeviceToHost, s));
+    HIP_CHECK(c, hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
     HIP_CHECK(c, hipStreamSynchronize(s));
-    for (int i = 0; i < k; ++i) drafts[i] = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[i + 1] & 0xFFFFFFFFull));
+    for (int i = 0; i < k; ++i) drafts[i] = key_token(key_value(c->keys_h, i + 1));
   }
   return LEDE_OK;
 }
@@ -917,7 +918,8 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
   int rc = from ? extend_drafts(c, from, k, s) : LEDE_OK;
   if (!rc) rc = launch_verify(c, k, s, 0.f, from);
   if (rc) return rc;
-  if (verify) HIP_CHECK(c, hipMemcpyAsync(c->keys_h + 16, c->S<uint64_t>(c->lo.vkeys), 16 * 8, hipMemcpyDeviceToHost, s));
+  if (verify)
+    HIP_CHECK(c, hipMemcpyAsync(c->keys_h + KEY_WORDS, c->S<uint64_t>(c->lo.vkeys), KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
   rc = read_record(c, s);
   if (rc) return rc;
   commit_host(c);
@@ -925,7 +927,7 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
   if (accepted) *accepted = a;
   if (n_emitted) *n_emitted = a + 1;
   if (tokens) for (int i = 0; i <= a; ++i) tokens[i] = c->record_h[4 + i];
-  if (verify) for (int i = 0; i <= k; ++i) verify[i] = (int)(0xFFFFFFFFu - (uint32_t)(c->keys_h[16 + i] & 0xFFFFFFFFull));
+  if (verify) for (int i = 0; i <= k; ++i) verify[i] = key_token(key_value(c->keys_h + KEY_WORDS, i));
   return LEDE_OK;
 }
 
@@ -1198,7 +1200,7 @@ int lede_op_sample(const float* logits, int32_t V, float temperature, float u, i
   if (!(temperature > 0.f) || !std::isfinite(temperature) || !(u >= 0.f && u < 1.f)) return LEDE_E_ARG;
   hipStream_t s = S_(stream);
   uint64_t* key = nullptr;
-  if (hipMalloc((void**)&key, 16) != hipSuccess) return LEDE_E_HIP;
+  if (hipMalloc((void**)&key, KEY_WORDS * 8) != hipSuccess) return LEDE_E_HIP;
   SampleArgs sa{};
   sa.logits = logits; sa.vocab = V; sa.inv_t = 1.f / temperature;
   sa.u = nullptr; sa.u_imm = u; sa.key_out = key; sa.stats_out = nullptr;
@@ -1208,7 +1210,7 @@ int lede_op_sample(const float* logits, int32_t V, float temperature, float u, i
       hipStreamSynchronize(s) != hipSuccess)
     rc = LEDE_E_HIP;
   (void)hipFree(key);
-  if (rc == LEDE_OK) *token = (int32_t)(0xFFFFFFFFu - (uint32_t)(h & 0xFFFFFFFFull));
+  if (rc == LEDE_OK) *token = key_token(h);  // a single writer: word 0 holds the key
   return rc;
 }
 
