@@ -37,6 +37,9 @@ class Report:
     max_err_abs: float = 0.0
     substitutions: int = 0
     steps: int = 0
+    # sampled steps: summed probability (over the shared uniforms) that a
+    # decision taken on the GPU's logits differs from the oracle's
+    expected_substitutions: float = 0.0
     notes: List[str] = field(default_factory=list)
 
     def row(self, dtype, z_gpu, z_orc):
@@ -177,6 +180,35 @@ def draw_consistent(w, v, u, delta):
     return lo - delta <= u <= hi + delta
 
 
+def draw_split(wa, wb):
+    """Probability over a shared uniform u that the inverse-CDF draws from
+    the weights wa and wb differ: the measure of the u for which they do.
+    Between consecutive points of the two CDFs both draws are constant."""
+    ca = np.cumsum(np.asarray(wa, dtype=np.float64))
+    cb = np.cumsum(np.asarray(wb, dtype=np.float64))
+    if not (ca[-1] > 0 and cb[-1] > 0):
+        return 1.0  # an empty residual: the draw falls back to another rule
+    ca, cb = ca / ca[-1], cb / cb[-1]
+    pts = np.unique(np.concatenate([[0.0, 1.0], ca, cb]))
+    mid = 0.5 * (pts[:-1] + pts[1:])
+    differ = np.searchsorted(ca, mid, side="right") != np.searchsorted(cb, mid, side="right")
+    return float(np.sum(np.diff(pts)[differ]))
+
+
+def near_tie_bound(mu, alpha=1e-3):
+    """Largest substitution count consistent at level alpha with decisions
+    whose divergence probabilities sum to mu: the Poisson(mu) upper quantile,
+    whose tail bounds that of any sum of independent Bernoulli variables with
+    that mean."""
+    n, term = 0, np.exp(-mu)
+    cdf = term
+    while 1.0 - cdf > alpha:
+        n += 1
+        term *= mu / n
+        cdf += term
+    return n
+
+
 def _spread(eps, T):
     """Bound on how far a CDF or a probability ratio moves when every logit
     moves by at most eps (softmax at temperature T)."""
@@ -228,6 +260,7 @@ def check_sampled(eng, st: SSDState, model, n_total, actions, T, rep: Report, st
             eps = max(eps, float(np.max(np.abs(zd[j] - st.last_draft_logits[j]))))
             g = rec.drafts[j]
             assert draw_consistent(om.probs_at(zd[j], T), g, u[j], CDF_EPS), ("draft draw", j)
+            rep.expected_substitutions += draw_split(om.probs_at(zd[j], T), st.last_q_rows[j])
             if g != orc.drafts[j]:
                 assert draw_consistent(st.last_q_rows[j], g, u[j], _spread(eps, T)), ("draft", j)
                 diverged = True
@@ -236,11 +269,17 @@ def check_sampled(eng, st: SSDState, model, n_total, actions, T, rep: Report, st
             for j in range(ke + 1):
                 rep.row(dt, zv[j], st.last_verify_logits[j])
                 eps = max(eps, float(np.max(np.abs(zv[j] - st.last_verify_logits[j]))))
-            a_g, w_g, _, _ = _decisions(zd, zv, rec.drafts, u, T)
+            a_g, w_g, p_g, q_g = _decisions(zd, zv, rec.drafts, u, T)
             assert a_g == rec.accepted, ("acceptance on the GPU's own logits", a_g, rec.accepted)
             assert draw_consistent(w_g, rec.emitted[-1], u[2 * om.SAMPLE_SLOTS], CDF_EPS), "final draw"
             a_o, w_o, p_o, q_o = _decisions(st.last_draft_logits, st.last_verify_logits, orc.drafts, u, T)
             assert a_o == orc.accepted
+            # acceptance tests up to the first rejection on either side: u < p / q
+            for j in range(min(a_g, a_o, ke - 1) + 1 if ke else 0):
+                d = orc.drafts[j]
+                rep.expected_substitutions += abs(min(1.0, p_g[j][d] / q_g[j][d]) - min(1.0, p_o[j][d] / q_o[j][d]))
+            if a_g == a_o:
+                rep.expected_substitutions += draw_split(w_g, w_o)
             if a_g != a_o:
                 j = min(a_g, a_o)
                 d = orc.drafts[j]
