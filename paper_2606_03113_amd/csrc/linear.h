@@ -121,7 +121,16 @@ struct LinearArgs {
   void* act; int ld_act;
   // EPI_ARGMAX
   uint64_t* keys; float* logits; int ld_logits; int vocab;
+  // RMSNorm of a multi-row pass split over two kernels.  A residual producer
+  // (EPI_RESID) with ss_out also stores xg[m][n] = h[m][n] * xg_gain[n] in the
+  // model dtype and, per 16-column group g, the sum of squares of its columns
+  // of each new residual row, ss_out[g * 16 + m].  A matrix-core consumer with
+  // ss_in reads x = xg and scales output row m by
+  // 1 / sqrt(sum over the ss_groups partials / K + eps).
+  float* ss_out; const void* xg_gain; void* xg; int ldxg;
+  const float* ss_in; int ss_groups;
 };
+constexpr int SS_MAX_GROUPS = 512;  // rows of up to 8192 elements
 
 // Linear kernel shape: wavefronts per block, and where the input row comes
 // from (see k_linear).  Rows longer than LIN_LDS_X_MAX bytes are read from

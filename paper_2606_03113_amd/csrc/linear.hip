@@ -75,7 +75,16 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
     }
     case EPI_RESID: {
       const int n = tid >> 4, m = tid & 15;
-      if (m < M) a.h[(size_t)m * a.ldh + g * 16 + n] += ct[n][m];
+      if (m < M) {
+        const int col = g * 16 + n;
+        float* hp = a.h + (size_t)m * a.ldh + col;
+        const float hn = *hp + ct[n][m];
+        *hp = hn;
+        if (a.ss_out) {
+          Elem<DT>::store(a.xg, (size_t)m * a.ldxg + col, hn * Elem<DT>::load(a.xg_gain, col));
+          ct[n][m] = hn;  // squared and summed per row once the block has synchronised
+        }
+      }
       break;
     }
     case EPI_SWIGLU: {
@@ -245,12 +254,28 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   __shared__ float red[NW][16][16];
   __shared__ float ct[16][17];
   __shared__ float scratch[NW];
+  __shared__ float inv_s[16];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int KT = a.KT, NG = a.n_groups;
   const uint4 zero = {0u, 0u, 0u, 0u};
 
   if (blockIdx.x == 0 && a.zero_keys && tid < KEY_WORDS && (tid % KEY_PITCH) < a.n_zero_keys) a.zero_keys[tid] = 0;
+
+  // split norm: the producer's partial sums are requested ahead of the
+  // weights, so that waiting for them does not wait for the weights
+  static_assert(NW * 64 == 512, "32 threads per row of partial sums");
+  constexpr int SSJ = SS_MAX_GROUPS / 32;
+  const bool split_norm = MFMA && a.ss_in;
+  float ssv[SSJ];
+  if (split_norm) {
+    const int m = tid & 15, j0 = tid >> 4;
+#pragma unroll
+    for (int i = 0; i < SSJ; ++i) {
+      const int j = j0 + 32 * i;
+      ssv[i] = (m < a.M && j < a.ss_groups) ? a.ss_in[j * 16 + m] : 0.f;
+    }
+  }
 
   int g = blockIdx.x;
   // the weights do not depend on the input: the first batch is in flight
@@ -267,6 +292,21 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   if (XS == XS_LDS) {
     if (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM) stage_norm_row<DT, NW>(a, smem, scratch);
     else stage_copy_row<NW>(a.x, KT * TL::TK * TL::ES, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
+  }
+  if (split_norm) {
+    // row m's sum: thread partials in i order, then the 32 threads in order
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < SSJ; ++i) s += ssv[i];
+    float* ssr = &red[0][0][0];  // [32][16], free until the main loop's partials
+    ssr[tid] = s;                // = ssr[j0 * 16 + m]
+    __syncthreads();
+    if (tid < 16) {
+      float t = 0.f;
+      for (int j = 0; j < 32; ++j) t += ssr[j * 16 + tid];
+      inv_s[tid] = rsqrtf(t / (float)a.K + a.eps);
+    }
+    __syncthreads();
   }
 
   uint64_t best = 0;
@@ -331,12 +371,18 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
         float s = red[0][n][mm];
 #pragma unroll
         for (int q = 1; q < NW; ++q) s += red[q][n][mm];
-        ct[n][mm] = s;
+        ct[n][mm] = split_norm ? s * inv_s[mm] : s;
       }
     }
     __syncthreads();
     if (tid < 256) epilogue<DT>(a, g, ct, best);
     __syncthreads();
+    if (a.epi == EPI_RESID && a.ss_out && tid < 16) {
+      float s = 0.f;
+      if (tid < a.M)
+        for (int n = 0; n < 16; ++n) s = fmaf(ct[n][tid], ct[n][tid], s);
+      a.ss_out[g * 16 + tid] = s;
+    }
   }
   if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
     atomicMax((unsigned long long*)&a.keys[(blockIdx.x % KEY_SLOTS) * KEY_PITCH + tid], (unsigned long long)best);

@@ -38,7 +38,7 @@ struct Layout {
   size_t embed, final_norm, head, qw1, qb1, qw2, qb2, ew1, eb1, ew2, eb2, wbytes;
   int He;  // exit-policy Q-network hidden width (0: none)
   // workspace offsets
-  size_t h, xn, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
+  size_t h, xn, ss, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
       record, rope, unif, dstats, trace, trace_state, pol_out, wsbytes;
   size_t kvbytes, kv_half;
 };
@@ -111,6 +111,7 @@ Layout make_layout(const lede_config* c) {
   off = 0;
   o.h = take((size_t)MROWS * o.d * 4);
   o.xn = take((size_t)MROWS * o.d * o.es);
+  o.ss = take((size_t)(o.d / 16) * 16 * 4);   // split-norm partial sums [d/16][16]
   o.q = take((size_t)MROWS * o.qd * 4);
   o.attn_out = take((size_t)MROWS * o.qd * o.es);
   o.act = take((size_t)MROWS * o.Fp * o.es);
@@ -304,6 +305,8 @@ double linear_bytes(const LinearArgs& a, int dt) {
     case EPI_ARGMAX: y = M * 8 + (a.logits ? M * N * 4 : 0); break;
     default: y = M * N * 4;
   }
+  if (a.ss_out) y += M * N * es + N * es + N / 16 * M * 4;  // h * gain, the gain, the partial sums
+  if (a.ss_in) x += (double)a.ss_groups * M * 4;
   return N * K * es + x + y;
 }
 
@@ -351,9 +354,25 @@ int linear_grid(int n_groups, int epi) {
 }
 
 // One-row passes normalise their input row in every block of the linear
-// kernel (the row is re-read from L2 by each block).  Multi-row passes use
-// the norm kernel, one block per row: re-reading k+1 residual rows in every
-// block of the matrix-core kernel costs more than the launch it saves.
+// kernel (the row is re-read from L2 by each block).  Multi-row passes split
+// each RMSNorm over the kernels around it: the residual producer before it
+// stores h * gain and per-group sums of squares, the matrix-core consumer
+// after it scales its output rows by the inverse RMS.  Only the first norm of
+// a pass, whose residual rows come from elsewhere (the embedding, or the
+// draft passes under verify reuse), runs the norm kernel.  Normalising in
+// every consumer block instead would re-read k+1 residual rows per block.
+
+// Arm a residual producer (EPI_RESID) to prepare the split norm with gain.
+void split_norm_produce(const lede_ctx* c, LinearArgs& a, const void* gain) {
+  a.ss_out = c->S<float>(c->lo.ss);
+  a.xg = c->S<void>(c->lo.xn); a.ldxg = c->lo.d;
+  a.xg_gain = gain;
+}
+// Feed a matrix-core consumer of width d from the split norm.
+void split_norm_consume(const lede_ctx* c, LinearArgs& a) {
+  a.x_mode = X_PLAIN; a.x = c->S<void>(c->lo.xn); a.ldx = c->lo.d;
+  a.ss_in = c->S<float>(c->lo.ss); a.ss_groups = c->lo.d / 16;
+}
 
 LinearArgs base_linear(const lede_ctx* c) {
   LinearArgs a{};
@@ -401,6 +420,8 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       qa.vocab = o.V;
       // the pass's argmax slots are cleared by its first kernel
       if (j == l_begin && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = vec ? 1 : M; }
+    } else if (j > l_begin) {
+      split_norm_consume(c, qa);  // prepared by the previous layer's down projection
     } else {
       NormArgs na{};
       na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
@@ -440,6 +461,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
     oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
     oa.epi = EPI_RESID;
+    if (!vec) split_norm_produce(c, oa, c->W<void>(lw.ffn_norm));
     LAUNCH_LINEAR(vec, oa, dt);
 
     // feed-forward block
@@ -452,12 +474,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     if (vec) {
       ga.x_mode = X_NORM; ga.gain = c->W<void>(lw.ffn_norm);
     } else {
-      NormArgs na{};
-      na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
-      na.h = c->S<float>(o.h); na.gain = c->W<void>(lw.ffn_norm); na.eps = c->cfg.rms_eps;
-      na.x = c->S<void>(o.xn);
-      LAUNCH(LEDE_K_NORM, (double)M * o.d * (4 + o.es), launch_norm(dt, na, s));
-      ga.x_mode = X_PLAIN; ga.x = c->S<void>(o.xn); ga.ldx = o.d;
+      split_norm_consume(c, ga);
     }
     LAUNCH_LINEAR(vec, ga, dt);
 
@@ -468,6 +485,10 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
     da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
     da.epi = EPI_RESID;
+    // the next norm: the next layer's attention norm, or the final norm when
+    // the pass ends at the last layer (the head follows)
+    if (!vec && j + 1 < l_end) split_norm_produce(c, da, c->W<void>(o.lay[j + 1].attn_norm));
+    else if (!vec && l_end == o.L) split_norm_produce(c, da, c->W<void>(o.final_norm));
     LAUNCH_LINEAR(vec, da, dt);
 
     if (qnet_after == j + 1 && o.H > 0) {
@@ -493,7 +514,9 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 }
 
 // Shared final RMSNorm + LM head + argmax for rows [0, M) into keys[0..M).
-int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s, int vec_row = 0) {
+// split: a multi-row pass through the last layer prepared the final norm.
+int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s, int vec_row = 0,
+             bool split = false) {
   const Layout& o = c->lo;
   LinearArgs ha = base_linear(c);
   ha.M = M;
@@ -504,6 +527,8 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   ha.logits = logits; ha.ld_logits = o.V;
   if (vec) {
     ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
+  } else if (split) {
+    split_norm_consume(c, ha);
   } else {
     NormArgs na{};
     na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
@@ -586,7 +611,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from
   } else if ((rc = run_layers(c, k + 1, false, tok, 0, from_layer, c->lo.L, 0, vk, s))) {
     return rc;
   }
-  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s);
+  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s, 0, from_layer < c->lo.L);
   if (rc) return rc;
   AcceptArgs aa{};
   aa.dkeys = dk; aa.vkeys = vk; aa.k = k;
@@ -828,7 +853,7 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
     rc = run_layers(c, M, false, tok, off, 0, c->lo.L, 0, vk, s);
     if (!rc && off + M == n) {
       const bool trace = c->lo.He > 0;
-      rc = run_head(c, M, false, vk, verify_logits(c, trace), s);
+      rc = run_head(c, M, false, vk, verify_logits(c, trace), s, 0, true);
       if (!rc && trace) rc = push_trace(c, verify_logits(c, true) + (size_t)(M - 1) * c->lo.V, 1, nullptr, s);
     }
     if (rc) { truncate_pages(c, c0); (void)saved_table; return rc; }
