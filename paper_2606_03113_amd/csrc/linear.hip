@@ -56,8 +56,30 @@ __global__ __launch_bounds__(256) void k_repack(RepackArgs a) {
 
 // ---- linear: y = W x with fused prologue / epilogue --------------------------
 
+// What the QKV epilogue of thread tid needs from the sequence length c
+// alone: the rotary pair of its (row, dim) in q / k groups and the cache page
+// of its row.  Fetched before the weights stream for the block's first group.
+struct QkvPre {
+  float2 cs;
+  int page;
+};
+__device__ __forceinline__ QkvPre qkv_fetch(const LinearArgs& a, int g, int c) {
+  const int tid = threadIdx.x, m = tid & 15;
+  const int gph = a.hd / 16, qg = a.nq * gph, kg = a.nkv * gph;
+  QkvPre p = {make_float2(1.f, 0.f), 0};
+  if (tid >= 256 || m >= a.M) return p;
+  const int pos = c + m;
+  if (g >= qg) p.page = a.block_table[pos >> 6];
+  if (g < qg + kg && tid < 128) {
+    const int gl = g < qg ? g : g - qg;
+    p.cs = a.rope[(size_t)pos * (a.hd / 2) + 8 * (gl % gph) + (tid >> 4)];
+  }
+  return p;
+}
+
 template <int DT>
-__device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best) {
+__device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best, int qkv_c,
+                                         const QkvPre& pre) {
   const int tid = threadIdx.x;
   const int M = a.M;
   switch (a.epi) {
@@ -101,7 +123,8 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
     case EPI_QKV: {
       const int hd = a.hd, gph = hd / 16;
       const int qg = a.nq * gph, kg = a.nkv * gph;
-      const int c = *a.seq_len + a.pos_off;
+      const int c = qkv_c;
+      const QkvPre p = g == (int)blockIdx.x ? pre : qkv_fetch(a, g, c);
       if (g < qg + kg) {
         if (tid < 128) {
           const int r = tid >> 4, m = tid & 15;
@@ -110,7 +133,7 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
             const int gl = isq ? g : g - qg;
             const int head = gl / gph, i = 8 * (gl % gph) + r;
             const int pos = c + m;
-            const float2 cs = a.rope[(size_t)pos * (hd / 2) + i];
+            const float2 cs = p.cs;
             const float x0 = ct[r][m], x1 = ct[r + 8][m];
             const float y0 = x0 * cs.x - x1 * cs.y;
             const float y1 = x1 * cs.x + x0 * cs.y;
@@ -119,8 +142,7 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
               q[i] = y0;
               q[i + hd / 2] = y1;
             } else {
-              const int page = a.block_table[pos >> 6];
-              const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+              const size_t base = ((((size_t)a.layer * a.n_pages + p.page) * a.nkv + head) * 64 + (pos & 63)) * hd;
               Elem<DT>::store(a.kcache, base + i, y0);
               Elem<DT>::store(a.kcache, base + i + hd / 2, y1);
             }
@@ -132,8 +154,7 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
           const int dim = (g - qg - kg) * 16 + n;
           const int head = dim / hd, i = dim % hd;
           const int pos = c + m;
-          const int page = a.block_table[pos >> 6];
-          const size_t base = ((((size_t)a.layer * a.n_pages + page) * a.nkv + head) * 64 + (pos & 63)) * hd;
+          const size_t base = ((((size_t)a.layer * a.n_pages + p.page) * a.nkv + head) * 64 + (pos & 63)) * hd;
           Elem<DT>::store(a.vcache, base + i, ct[n][m]);
         }
       }
@@ -177,37 +198,50 @@ __device__ __forceinline__ float block_sum(float v, float* scratch) {
 // thread of the block: thread t holds elements 4t + 4 NT j of the row and of
 // the gain in registers (both requested together), sums the squares in j
 // order, and the block sums the threads' partials in wave order.  The row is
-// zero-padded to the batch size the main loop reads.
+// zero-padded to the batch size the main loop reads.  The loads are issued
+// before the first weight batch (norm_row_load) and consumed after it
+// (norm_row_stage): vector loads complete in issue order, so waiting for the
+// row then does not wait for the weights.
+template <int NW>
+struct NormRow {
+  static constexpr int NT = NW * 64, J = (8192 + 4 * NT - 1) / (4 * NT);  // rows of up to 8192 elements
+  float4 v[J], g[J];
+};
+
 template <int DT, int NW>
-__device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch) {
-  constexpr int NT = NW * 64, J = (8192 + 4 * NT - 1) / (4 * NT);  // rows of up to 8192 elements
+__device__ __forceinline__ void norm_row_load(const LinearArgs& a, NormRow<NW>& nr) {
+  constexpr int NT = NormRow<NW>::NT, J = NormRow<NW>::J;
   const int tid = threadIdx.x;
-  const int row_bytes = a.K * Elem<DT>::ES_, pad_bytes = lin_x_tiles(a.KT) * Tile<DT>::TK * Elem<DT>::ES_;
-  for (int i = row_bytes + tid * 4; i < pad_bytes; i += NT * 4) *(uint32_t*)(lds + i) = 0u;
   const float* h = a.h;
   const void* row = nullptr;
-  float* h_out = nullptr;
   if (a.x_mode == X_EMBED_NORM) {
     const int tok = (int)min((unsigned)a.tok.get(0), (unsigned)(a.vocab - 1));
     row = (const uint8_t*)a.embed + (size_t)tok * a.K * Elem<DT>::ES_;
-    if (blockIdx.x == 0) h_out = a.h;
     h = nullptr;
   }
-  float4 v[J], g[J];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int i = 4 * tid + 4 * NT * j;
     const bool in = i < a.K;
-    v[j] = in ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    g[j] = in ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    nr.v[j] = in ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    nr.g[j] = in ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
+}
+
+template <int DT, int NW>
+__device__ void norm_row_stage(const LinearArgs& a, const NormRow<NW>& nr, uint8_t* lds, float* scratch) {
+  constexpr int NT = NormRow<NW>::NT, J = NormRow<NW>::J;
+  const int tid = threadIdx.x;
+  const int row_bytes = a.K * Elem<DT>::ES_, pad_bytes = lin_x_tiles(a.KT) * Tile<DT>::TK * Elem<DT>::ES_;
+  for (int i = row_bytes + tid * 4; i < pad_bytes; i += NT * 4) *(uint32_t*)(lds + i) = 0u;
+  float* h_out = (a.x_mode == X_EMBED_NORM && blockIdx.x == 0) ? a.h : nullptr;
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    ss = fmaf(v[j].x, v[j].x, ss);
-    ss = fmaf(v[j].y, v[j].y, ss);
-    ss = fmaf(v[j].z, v[j].z, ss);
-    ss = fmaf(v[j].w, v[j].w, ss);
+    ss = fmaf(nr.v[j].x, nr.v[j].x, ss);
+    ss = fmaf(nr.v[j].y, nr.v[j].y, ss);
+    ss = fmaf(nr.v[j].z, nr.v[j].z, ss);
+    ss = fmaf(nr.v[j].w, nr.v[j].w, ss);
   }
   ss = block_sum<NW>(ss, scratch);
   const float inv = rsqrtf(ss / (float)a.K + a.eps);
@@ -216,11 +250,11 @@ __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch
     const int i = 4 * tid + 4 * NT * j;
     if (i < a.K) {
       float4 y;
-      y.x = (v[j].x * inv) * g[j].x;
-      y.y = (v[j].y * inv) * g[j].y;
-      y.z = (v[j].z * inv) * g[j].z;
-      y.w = (v[j].w * inv) * g[j].w;
-      if (h_out) *(float4*)(h_out + i) = v[j];
+      y.x = (nr.v[j].x * inv) * nr.g[j].x;
+      y.y = (nr.v[j].y * inv) * nr.g[j].y;
+      y.z = (nr.v[j].z * inv) * nr.g[j].z;
+      y.w = (nr.v[j].w * inv) * nr.g[j].w;
+      if (h_out) *(float4*)(h_out + i) = nr.v[j];
       store4<DT>(lds, i, y);
     }
   }
@@ -228,11 +262,30 @@ __device__ void stage_norm_row(const LinearArgs& a, uint8_t* lds, float* scratch
 }
 
 // Copy the vector kernel's input row (KT tiles of the model dtype) into LDS
-// and zero the padding up to pad bytes.
+// and zero the padding up to pad bytes; loaded before the first weight batch
+// (copy_row_load), stored after it (copy_row_stage), like the normalised row.
 template <int NW>
-__device__ void stage_copy_row(const void* x, int bytes, int pad, uint8_t* lds) {
-  for (int i = threadIdx.x * 16; i < pad; i += NW * 64 * 16)
-    *(uint4*)(lds + i) = i < bytes ? ld16((const uint8_t*)x + i) : make_uint4(0u, 0u, 0u, 0u);
+struct CopyRow {
+  static constexpr int C = LIN_LDS_X_MAX / (NW * 64 * 16);  // 16-byte chunks per thread
+  uint4 c[C];
+};
+
+template <int NW>
+__device__ __forceinline__ void copy_row_load(const void* x, int bytes, CopyRow<NW>& cr) {
+#pragma unroll
+  for (int u = 0; u < CopyRow<NW>::C; ++u) {
+    const int i = (threadIdx.x + NW * 64 * u) * 16;
+    cr.c[u] = i < bytes ? ld16((const uint8_t*)x + i) : make_uint4(0u, 0u, 0u, 0u);
+  }
+}
+
+template <int NW>
+__device__ void copy_row_stage(const CopyRow<NW>& cr, int pad, uint8_t* lds) {
+#pragma unroll
+  for (int u = 0; u < CopyRow<NW>::C; ++u) {
+    const int i = (threadIdx.x + NW * 64 * u) * 16;
+    if (i < pad) *(uint4*)(lds + i) = cr.c[u];
+  }
   __syncthreads();
 }
 
@@ -277,6 +330,15 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     }
   }
 
+  // QKV: the sequence length is requested first (a scalar load, waited for
+  // only after the weights are issued)
+  const int qkv_c = a.epi == EPI_QKV ? *a.seq_len + a.pos_off : 0;
+  const bool norm_row = XS == XS_LDS && (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM);
+  NormRow<NW> nrow;
+  CopyRow<NW> crow;
+  if (norm_row) norm_row_load<DT, NW>(a, nrow);
+  else if (XS == XS_LDS) copy_row_load<NW>(a.x, KT * TL::TK * TL::ES, crow);
+
   int g = blockIdx.x;
   // the weights do not depend on the input: the first batch is in flight
   // while the prologue stages the input row
@@ -290,8 +352,8 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     }
   }
   if (XS == XS_LDS) {
-    if (a.x_mode == X_NORM || a.x_mode == X_EMBED_NORM) stage_norm_row<DT, NW>(a, smem, scratch);
-    else stage_copy_row<NW>(a.x, KT * TL::TK * TL::ES, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
+    if (norm_row) norm_row_stage<DT, NW>(a, nrow, smem, scratch);
+    else copy_row_stage<NW>(crow, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
   }
   if (split_norm) {
     // row m's sum: thread partials in i order, then the 32 threads in order
@@ -308,6 +370,9 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     }
     __syncthreads();
   }
+
+  QkvPre qpre = {make_float2(1.f, 0.f), 0};
+  if (a.epi == EPI_QKV) qpre = qkv_fetch(a, blockIdx.x, qkv_c);
 
   uint64_t best = 0;
   bool first = true;
@@ -375,7 +440,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
       }
     }
     __syncthreads();
-    if (tid < 256) epilogue<DT>(a, g, ct, best);
+    if (tid < 256) epilogue<DT>(a, g, ct, best, qkv_c, qpre);
     __syncthreads();
     if (a.epi == EPI_RESID && a.ss_out && tid < 16) {
       float s = 0.f;
