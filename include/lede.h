@@ -368,7 +368,7 @@ int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats
  * weights and KV read once, plus activations in and out. */
 enum {
   LEDE_K_LINEAR_VEC = 0,  /* one-row linear kernel, input row staged in LDS (draft path) */
-  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel (verify / prefill path) */
+  LEDE_K_LINEAR_MFMA,     /* matrix-core linear kernel, input rows read from global memory (verify / prefill path) */
   LEDE_K_ATTENTION,       /* paged attention partial + combine */
   LEDE_K_NORM,            /* RMSNorm rows */
   LEDE_K_QNET,            /* Q-network layers */
@@ -376,6 +376,7 @@ enum {
   LEDE_K_DRAFT_PHASE,     /* all draft passes of a step */
   LEDE_K_VERIFY_PHASE,    /* the verify pass + acceptance of a step */
   LEDE_K_LINEAR_VEC_GX,   /* one-row linear kernel, input row read from global memory (rows > 32 KiB) */
+  LEDE_K_LINEAR_MFMA_LX,  /* matrix-core linear kernel, input rows staged in LDS (all rows <= 48 KiB) */
   LEDE_K_NCLASS
 };
 typedef struct {

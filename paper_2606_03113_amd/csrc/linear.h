@@ -138,14 +138,17 @@ constexpr int SS_MAX_GROUPS = 512;  // rows of up to 8192 elements
 constexpr int LIN_WAVES = 8;
 constexpr int LIN_LDS_X_MAX = 32768;
 constexpr int LIN_TILES_PER_WAVE = 4;  // tiles each wavefront has in flight per batch
-enum XSource { XS_LDS = 0, XS_GLOBAL = 1, XS_MFMA = 2 };
+enum XSource { XS_LDS = 0, XS_GLOBAL = 1, XS_MFMA = 2, XS_MFMA_LDS = 3 };
+// Matrix-core input rows are staged in LDS when they take at most this many
+// bytes (three blocks of 512 threads still fit a CU's 160 KiB).
+constexpr int LIN_MFMA_LDS_X_MAX = 48 * 1024;
 // K tiles the staged row is zero-padded to, so that every batch reads it
 // without bounds checks.
 __host__ __device__ inline int lin_x_tiles(int KT) {
   const int b = LIN_WAVES * LIN_TILES_PER_WAVE;
   return (KT + b - 1) / b * b;
 }
-int linear_x_source(int dtype, bool mfma, int K);
+int linear_x_source(int dtype, bool mfma, int K, int M);
 
 // Bytes of dynamic LDS the linear kernels use for the staged input row.
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M);

@@ -179,6 +179,14 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
 }
 
 
+// 16 bytes from LDS through an LDS-typed pointer: a select between such a
+// load and a register constant cannot become a load through a selected
+// pointer (which would put the constant in scratch memory).
+__device__ __forceinline__ uint4 lds_ld16(const uint8_t* p) {
+  const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Deterministic sum over the NW wavefronts of a block (every thread takes
 // part in the barriers).
 template <int NW>
@@ -296,13 +304,20 @@ __device__ void copy_row_stage(const CopyRow<NW>& cr, int pad, uint8_t* lds) {
 //                   for X_NORM / X_EMBED_NORM, copied otherwise); dot2 math.
 //   XS = XS_GLOBAL: one input row read from global memory per tile (rows too
 //                   long for LDS); dot2 math.
-//   XS = XS_MFMA:   up to 16 rows read from global memory (normalised by the
-//                   norm kernel), 16x16 matrix-core tiles.
+//   XS = XS_MFMA:   up to 16 rows read from global memory per tile, 16x16
+//                   matrix-core tiles.
+//   XS = XS_MFMA_LDS: the same, with the rows staged in LDS in the prologue:
+//                   each wavefront copies the tiles it will use (direct
+//                   global-to-LDS loads issued before its weights) into a
+//                   region of its own, [row m][tile j][64 bytes], so that it
+//                   waits for its own loads only.
 template <int DT, int XS>
 __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   typedef Tile<DT> TL;
   constexpr int NW = LIN_WAVES, U = 4;  // tiles per wave per batch
-  constexpr bool MFMA = XS == XS_MFMA;
+  constexpr bool MFMA = XS == XS_MFMA || XS == XS_MFMA_LDS;
+  constexpr bool XL = XS == XS_MFMA_LDS;
+  static_assert(TL::TK * TL::ES == 64, "64 bytes of a row per tile");
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ float red[NW][16][16];
   __shared__ float ct[16][17];
@@ -314,6 +329,23 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   const uint4 zero = {0u, 0u, 0u, 0u};
 
   if (blockIdx.x == 0 && a.zero_keys && tid < KEY_WORDS && (tid % KEY_PITCH) < a.n_zero_keys) a.zero_keys[tid] = 0;
+
+  // staged matrix-core rows: 16 (row, tile) units of 64 bytes per load
+  // instruction, lane L carrying bytes 16 (L & 3) of unit L >> 2; a region
+  // holds xj tiles per row (a wavefront with fewer leaves the rest unused)
+  const int xj = (KT + NW - 1) / NW;                                    // tiles per row of a region
+  uint8_t* xw = smem + (size_t)wave * xj * a.M * (TL::TK * TL::ES);     // this wavefront's region
+  if (XL) {
+    const int jw = (KT - wave + NW - 1) / NW, units = xj * a.M;
+    for (int i = 0; i * 16 < units; ++i) {
+      const int u = i * 16 + (lane >> 2);
+      const int m = u / xj, j = u - m * xj;
+      const uint8_t* src = (const uint8_t*)a.x + ((size_t)m * a.ldx * TL::ES + (size_t)(wave + NW * j) * 64 + (lane & 3) * 16);
+      if (u < units && j < jw)
+        __builtin_amdgcn_global_load_lds((const void*)src, (__attribute__((address_space(3))) void*)(xw + i * 1024), 16,
+                                         0, 0);
+    }
+  }
 
   // split norm: the producer's partial sums are requested ahead of the
   // weights, so that waiting for them does not wait for the weights
@@ -373,6 +405,10 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
 
   QkvPre qpre = {make_float2(1.f, 0.f), 0};
   if (a.epi == EPI_QKV) qpre = qkv_fetch(a, blockIdx.x, qkv_c);
+  // the staged rows: the compiler does not track the direct-to-LDS loads,
+  // so the wavefront waits for all of its loads (its first weight batch is
+  // needed by the first tile anyway)
+  if (XL) __builtin_amdgcn_s_waitcnt(0);
 
   uint64_t best = 0;
   bool first = true;
@@ -384,7 +420,10 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     const bool has = !MFMA || m < a.M;
     const uint8_t* xg = (const uint8_t*)a.x + ((size_t)m * a.ldx + (lane >> 4) * TL::EPL) * TL::ES;
     const uint8_t* xs = smem + (lane >> 4) * 16;
-    for (int t = wave; t < KT; t += NW * U) {
+    // staged rows: tile j of this lane's row at LDS byte xl + 64 j
+    const uint32_t xl = (uint32_t)(xw - smem) + m * xj * 64 + (lane >> 4) * 16;
+    int xrow0 = 0;
+    for (int t = wave; t < KT; t += NW * U, xrow0 += U) {
       if (!(first && t == wave)) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -406,7 +445,11 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
           const int tt = t + NW * u;
-          x[u] = (has && tt < KT) ? ld16(xg + (size_t)tt * TL::TK * TL::ES) : zero;
+          if (XL) {
+            x[u] = (has && tt < KT) ? lds_ld16(smem + xl + (uint32_t)(xrow0 + u) * 64) : zero;
+          } else {
+            x[u] = (has && tt < KT) ? ld16(xg + (size_t)tt * TL::TK * TL::ES) : zero;
+          }
         }
 #pragma unroll
         for (int u = 0; u < U; u += 2) {
@@ -463,19 +506,26 @@ hipError_t launch_repack(int dtype, const RepackArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-int linear_x_source(int dtype, bool mfma, int K) {
-  if (mfma) return XS_MFMA;
+// LDS bytes of matrix-core rows staged per wavefront region.
+static size_t mfma_lds_bytes(int dtype, int K, int M) {
+  const int tk = dtype == 1 ? 32 : 16;
+  const int KT = (K + tk - 1) / tk;
+  return (size_t)LIN_WAVES * ((KT + LIN_WAVES - 1) / LIN_WAVES) * M * 64;
+}
+
+int linear_x_source(int dtype, bool mfma, int K, int M) {
+  if (mfma) return mfma_lds_bytes(dtype, K, M) <= LIN_MFMA_LDS_X_MAX ? XS_MFMA_LDS : XS_MFMA;
   const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
   return (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es <= LIN_LDS_X_MAX ? XS_LDS : XS_GLOBAL;
 }
 
 size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
-  (void)M;
-  if (linear_x_source(dtype, mfma, K) != XS_LDS) return 0;
-  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
-  const size_t row = (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es;
   (void)x_mode;
-  return row;
+  const int xs = linear_x_source(dtype, mfma, K, M);
+  if (xs == XS_MFMA_LDS) return mfma_lds_bytes(dtype, K, M);
+  if (xs != XS_LDS) return 0;
+  const int tk = dtype == 1 ? 32 : 16, es = dtype == 1 ? 2 : 4;
+  return (size_t)lin_x_tiles((K + tk - 1) / tk) * tk * es;
 }
 
 // With events, the start / stop timestamps are taken by the dispatch itself
@@ -492,13 +542,15 @@ static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream
 hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s, hipEvent_t e0,
                          hipEvent_t e1) {
   const size_t lds = linear_lds_bytes(dtype, mfma, a.x_mode, a.K, a.M);
-  const int xs = linear_x_source(dtype, mfma, a.K);
+  const int xs = linear_x_source(dtype, mfma, a.K, a.M);
   if (dtype == 1) {
-    if (xs == XS_MFMA) launch_linear_t<1, XS_MFMA>(a, grid, lds, s, e0, e1);
+    if (xs == XS_MFMA_LDS) launch_linear_t<1, XS_MFMA_LDS>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_MFMA) launch_linear_t<1, XS_MFMA>(a, grid, lds, s, e0, e1);
     else if (xs == XS_LDS) launch_linear_t<1, XS_LDS>(a, grid, lds, s, e0, e1);
     else launch_linear_t<1, XS_GLOBAL>(a, grid, lds, s, e0, e1);
   } else {
-    if (xs == XS_MFMA) launch_linear_t<0, XS_MFMA>(a, grid, lds, s, e0, e1);
+    if (xs == XS_MFMA_LDS) launch_linear_t<0, XS_MFMA_LDS>(a, grid, lds, s, e0, e1);
+    else if (xs == XS_MFMA) launch_linear_t<0, XS_MFMA>(a, grid, lds, s, e0, e1);
     else if (xs == XS_LDS) launch_linear_t<0, XS_LDS>(a, grid, lds, s, e0, e1);
     else launch_linear_t<0, XS_GLOBAL>(a, grid, lds, s, e0, e1);
   }

@@ -266,18 +266,20 @@ int launch_linear_timed(lede_ctx* c, int cls, double bytes, int dt, bool mfma, c
   return LEDE_OK;
 }
 
-#define LAUNCH_LINEAR(vec, a, dt)                                                                        \
-  do {                                                                                                   \
-    int rc_ = launch_linear_timed(c, linear_class(dt, vec, (a).K), linear_bytes(a, dt), dt, !(vec), a,    \
-                                  linear_grid((a).n_groups, (a).epi), s);                               \
-    if (rc_) return rc_;                                                                                 \
+#define LAUNCH_LINEAR(vec, a, dt)                                                                  \
+  do {                                                                                             \
+    const int grid_ = linear_grid((a).n_groups, 16.0 * (a).K * ((dt) == 1 ? 2 : 4));               \
+    int rc_ = launch_linear_timed(c, linear_class(dt, vec, (a).K, (a).M), linear_bytes(a, dt), dt, \
+                                  !(vec), a, grid_, s);                                            \
+    if (rc_) return rc_;                                                                           \
   } while (0)
 
 // Timing class of a linear launch: one per kernel symbol.
-int linear_class(int dt, bool vec, int K) {
-  switch (linear_x_source(dt, !vec, K)) {
+int linear_class(int dt, bool vec, int K, int M) {
+  switch (linear_x_source(dt, !vec, K, M)) {
     case XS_LDS: return LEDE_K_LINEAR_VEC;
     case XS_GLOBAL: return LEDE_K_LINEAR_VEC_GX;
+    case XS_MFMA_LDS: return LEDE_K_LINEAR_MFMA_LX;
     default: return LEDE_K_LINEAR_MFMA;
   }
 }
@@ -346,11 +348,32 @@ int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
 
 // ---- pass orchestration -----------------------------------------------------------
 
-int linear_grid(int n_groups, int epi) {
-  // one 16-row group per block; the argmax head (2000 groups for a 32000-token
-  // vocabulary) runs faster with 1024 blocks taking two groups each than with
-  // 2000 blocks in two waves (46.3 vs 49.9 us measured)
-  return epi == EPI_ARGMAX ? std::min(n_groups, 1024) : n_groups;
+// Blocks of a linear launch (block b takes groups b, b + grid, ...), from a
+// time model fitted to cold-weight measurements: the busiest CU streams its
+// groups at about 19 GB/s with one resident block and 25 GB/s with two or
+// more (3 blocks of 512 threads fit a CU), and each round of resident blocks
+// costs about 1.6 us of ramp.  Ties go to fewer blocks.  It reproduces the
+// measured best choices for the 7B shapes: gate-up 1376 groups in 459
+// blocks (28.5 against 30.5 us in 1376), head 2000 groups in 500 blocks
+// (41.0 against 42.1 us in 1000), QKV (768) and the 256-group projections
+// at one group per block.
+int linear_grid(int n_groups, double group_bytes) {
+  constexpr int CUS = 256, RESIDENT = 3, GMAX = 16;
+  constexpr double RATE1 = 19.0e3, RATE2 = 25.0e3;  // bytes per us per CU
+  constexpr double RAMP_US = 1.6;
+  int best = 1;
+  double best_t = 0.0;
+  for (int G = 1; G <= GMAX && G <= n_groups; ++G) {
+    const int blocks = (n_groups + G - 1) / G;
+    const int per_cu = (blocks + CUS - 1) / CUS;
+    const int rounds = (per_cu + RESIDENT - 1) / RESIDENT;
+    const double t = (double)per_cu * G * group_bytes / (per_cu >= 2 ? RATE2 : RATE1) + rounds * RAMP_US;
+    if (G == 1 || t <= best_t) {
+      best = G;
+      best_t = t;
+    }
+  }
+  return (n_groups + best - 1) / best;
 }
 
 // One-row passes normalise their input row in every block of the linear

@@ -42,12 +42,12 @@ class LedeProfEntry(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double), ("bytes", ctypes.c_double), ("launches", ctypes.c_int64)]
 
 
-K_NCLASS = 9
+K_NCLASS = 10
 K_NAMES = ["linear_vec", "linear_mfma", "attention", "norm", "qnet", "accept", "draft_phase", "verify_phase",
-           "linear_vec_gx"]
+           "linear_vec_gx", "linear_mfma_lx"]
 # rocprofv3 kernel symbol of each linear timing class (bf16 models)
 K_SYMBOLS = {"linear_vec": "lede::k_linear<1, 0>", "linear_mfma": "lede::k_linear<1, 2>",
-             "linear_vec_gx": "lede::k_linear<1, 1>"}
+             "linear_vec_gx": "lede::k_linear<1, 1>", "linear_mfma_lx": "lede::k_linear<1, 3>"}
 
 
 class LedeAction(ctypes.Structure):
