@@ -121,12 +121,13 @@ struct LinearArgs {
   void* act; int ld_act;
   // EPI_ARGMAX
   uint64_t* keys; float* logits; int ld_logits; int vocab;
-  // RMSNorm of a multi-row pass split over two kernels.  A residual producer
-  // (EPI_RESID) with ss_out also stores xg[m][n] = h[m][n] * xg_gain[n] in the
-  // model dtype and, per 16-column group g, the sum of squares of its columns
-  // of each new residual row, ss_out[g * 16 + m].  A matrix-core consumer with
-  // ss_in reads x = xg and scales output row m by
-  // 1 / sqrt(sum over the ss_groups partials / K + eps).
+  // RMSNorm split over two kernels.  A residual producer (EPI_RESID) with
+  // ss_out also stores xg[m][n] = h[m][n] * xg_gain[n] in the model dtype and,
+  // per 16-column group g of its n_groups, the sum of squares of its columns
+  // of each new residual row, ss_out[m * n_groups + g] (rows 0..15).  A
+  // consumer with ss_in (the matrix-core kernel, or the one-row kernel with
+  // x_mode X_PLAIN) reads x = xg and scales output row m by
+  // 1 / sqrt(sum over the ss_groups partials of row m / K + eps).
   float* ss_out; const void* xg_gain; void* xg; int ldxg;
   const float* ss_in; int ss_groups;
 };

@@ -206,10 +206,9 @@ __device__ __forceinline__ float block_sum(float v, float* scratch) {
 // thread of the block: thread t holds elements 4t + 4 NT j of the row and of
 // the gain in registers (both requested together), sums the squares in j
 // order, and the block sums the threads' partials in wave order.  The row is
-// zero-padded to the batch size the main loop reads.  The loads are issued
-// before the first weight batch (norm_row_load) and consumed after it
-// (norm_row_stage): vector loads complete in issue order, so waiting for the
-// row then does not wait for the weights.
+// zero-padded to the batch size the main loop reads.  The loads
+// (norm_row_load) are issued together with the block's other prologue loads
+// and consumed (norm_row_stage) before the weights are requested.
 template <int NW>
 struct NormRow {
   static constexpr int NT = NW * 64, J = (8192 + 4 * NT - 1) / (4 * NT);  // rows of up to 8192 elements
@@ -270,8 +269,8 @@ __device__ void norm_row_stage(const LinearArgs& a, const NormRow<NW>& nr, uint8
 }
 
 // Copy the vector kernel's input row (KT tiles of the model dtype) into LDS
-// and zero the padding up to pad bytes; loaded before the first weight batch
-// (copy_row_load), stored after it (copy_row_stage), like the normalised row.
+// and zero the padding up to pad bytes, loaded (copy_row_load) and stored
+// (copy_row_stage) like the normalised row.
 template <int NW>
 struct CopyRow {
   static constexpr int C = LIN_LDS_X_MAX / (NW * 64 * 16);  // 16-byte chunks per thread
@@ -311,8 +310,9 @@ __device__ void copy_row_stage(const CopyRow<NW>& cr, int pad, uint8_t* lds) {
 //                   global-to-LDS loads issued before its weights) into a
 //                   region of its own, [row m][tile j][64 bytes], so that it
 //                   waits for its own loads only.
+// Six waves per SIMD (at most 80 VGPRs) keeps three blocks per CU.
 template <int DT, int XS>
-__global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
+__global__ __launch_bounds__(LIN_WAVES * 64) __attribute__((amdgpu_waves_per_eu(6))) void k_linear(LinearArgs a) {
   typedef Tile<DT> TL;
   constexpr int NW = LIN_WAVES, U = 4;  // tiles per wave per batch
   constexpr bool MFMA = XS == XS_MFMA || XS == XS_MFMA_LDS;
@@ -347,18 +347,22 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
     }
   }
 
-  // split norm: the producer's partial sums are requested ahead of the
-  // weights, so that waiting for them does not wait for the weights
-  static_assert(NW * 64 == 512, "32 threads per row of partial sums");
+  // split norm: the producer's partial sums, requested with the rows (vector
+  // loads complete in issue order: a wait for a load issued after the first
+  // weight batch would wait for the weights too)
+  static_assert(NW * 64 == 512 && SS_MAX_GROUPS <= 512, "32 threads per row of partial sums; one per thread");
   constexpr int SSJ = SS_MAX_GROUPS / 32;
-  const bool split_norm = MFMA && a.ss_in;
+  const bool split_norm = (MFMA || XS == XS_LDS) && a.ss_in;
   float ssv[SSJ];
   if (split_norm) {
-    const int m = tid & 15, j0 = tid >> 4;
+    if (MFMA) {
+      const int m = tid & 15, j0 = tid >> 4;
+      const float* row = a.ss_in + (m < a.M ? m : 0) * a.ss_groups;
+      const int nj = m < a.M ? a.ss_groups : 0;
 #pragma unroll
-    for (int i = 0; i < SSJ; ++i) {
-      const int j = j0 + 32 * i;
-      ssv[i] = (m < a.M && j < a.ss_groups) ? a.ss_in[j * 16 + m] : 0.f;
+      for (int i = 0; i < SSJ; ++i) ssv[i] = j0 + 32 * i < nj ? row[j0 + 32 * i] : 0.f;
+    } else {  // one row: thread t holds group t's partial
+      ssv[0] = tid < a.ss_groups ? a.ss_in[tid] : 0.f;
     }
   }
 
@@ -372,8 +376,16 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
   else if (XS == XS_LDS) copy_row_load<NW>(a.x, KT * TL::TK * TL::ES, crow);
 
   int g = blockIdx.x;
-  // the weights do not depend on the input: the first batch is in flight
-  // while the prologue stages the input row
+  // The input rows are staged before the first weight batch is requested.
+  // Every block starts within about 0.6 us, and a row requested alongside
+  // the weights waits behind every block's first batch: its first read
+  // misses the L2 (the previous kernel wrote it).  Waiting for the rows
+  // first and then streaming measured 5.756 against 5.774 ms per step.
+  if (XS == XS_LDS) {
+    if (norm_row) norm_row_stage<DT, NW>(a, nrow, smem, scratch);
+    else copy_row_stage<NW>(crow, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
+  }
+  if (XL) __builtin_amdgcn_s_waitcnt(0);  // this wavefront's staged tiles (and partial sums)
   uint4 w[U];
   {
     const uint8_t* wg = a.w + (size_t)(g < NG ? g : 0) * KT * TILE_BYTES + lane * 16;
@@ -383,11 +395,11 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
       w[u] = (g < NG && t < KT) ? ld16_stream(wg + (size_t)t * TILE_BYTES) : zero;
     }
   }
-  if (XS == XS_LDS) {
-    if (norm_row) norm_row_stage<DT, NW>(a, nrow, smem, scratch);
-    else copy_row_stage<NW>(crow, lin_x_tiles(KT) * TL::TK * TL::ES, smem);
-  }
-  if (split_norm) {
+  if (split_norm && !MFMA) {
+    const float t = block_sum<NW>(ssv[0], scratch);  // wave order
+    if (tid == 0) inv_s[0] = rsqrtf(t / (float)a.K + a.eps);
+    __syncthreads();
+  } else if (split_norm) {
     // row m's sum: thread partials in i order, then the 32 threads in order
     float s = 0.f;
 #pragma unroll
@@ -405,10 +417,8 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
 
   QkvPre qpre = {make_float2(1.f, 0.f), 0};
   if (a.epi == EPI_QKV) qpre = qkv_fetch(a, blockIdx.x, qkv_c);
-  // the staged rows: the compiler does not track the direct-to-LDS loads,
-  // so the wavefront waits for all of its loads (its first weight batch is
-  // needed by the first tile anyway)
-  if (XL) __builtin_amdgcn_s_waitcnt(0);
+  // the staged rows: the compiler does not track the direct-to-LDS loads
+  // (waited for above, before the weights were requested)
 
   uint64_t best = 0;
   bool first = true;
@@ -489,7 +499,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_linear(LinearArgs a) {
       float s = 0.f;
       if (tid < a.M)
         for (int n = 0; n < 16; ++n) s = fmaf(ct[n][tid], ct[n][tid], s);
-      a.ss_out[g * 16 + tid] = s;
+      a.ss_out[tid * NG + g] = s;
     }
   }
   if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)

@@ -164,6 +164,7 @@ struct lede_ctx {
   uint64_t* keys_h = nullptr;   // pinned read-back of argmax keys
   int use_graphs = 0, debug = 0;
   int verify_reuse = 0;  // verify from the exit layer on the draft passes' hidden states and KV
+  int split_row = -1;    // the one-row residual row whose final-norm split the last pass prepared
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
@@ -377,13 +378,17 @@ int linear_grid(int n_groups, double group_bytes) {
 }
 
 // One-row passes normalise their input row in every block of the linear
-// kernel (the row is re-read from L2 by each block).  Multi-row passes split
-// each RMSNorm over the kernels around it: the residual producer before it
-// stores h * gain and per-group sums of squares, the matrix-core consumer
-// after it scales its output rows by the inverse RMS.  Only the first norm of
-// a pass, whose residual rows come from elsewhere (the embedding, or the
-// draft passes under verify reuse), runs the norm kernel.  Normalising in
-// every consumer block instead would re-read k+1 residual rows per block.
+// Every RMSNorm after the first of a pass is split over the kernels around
+// it: the residual producer before it stores h * gain and per-group sums of
+// squares, the consumer after it reads h * gain as its input and scales its
+// output rows by the inverse RMS.  The first norm of a pass, whose residual
+// rows come from elsewhere (the embedding, an earlier segment of the exit
+// policy's pass, or the draft passes under verify reuse), normalises in the
+// one-row kernel's prologue or runs the norm kernel for several rows.  A
+// consumer that normalised in its own prologue would wait for the fp32
+// residual row and the gain before its first tile, behind the weight stream
+// of every other block; one that normalised several rows per block would
+// re-read k+1 residual rows in every block.
 
 // Arm a residual producer (EPI_RESID) to prepare the split norm with gain.
 void split_norm_produce(const lede_ctx* c, LinearArgs& a, const void* gain) {
@@ -435,16 +440,16 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     qa.layer = j; qa.n_pages = o.n_pages; qa.nq = o.nq; qa.nkv = o.nkv; qa.hd = o.hd;
     qa.block_table = c->S<int32_t>(o.btab); qa.seq_len = c->S<int32_t>(o.seq_len); qa.pos_off = pos_off;
     qa.rope = c->S<float2>(o.rope);
-    if (vec) {
+    if (j > l_begin) {
+      split_norm_consume(c, qa);  // prepared by the previous layer's down projection
+    } else if (vec) {
       qa.x_mode = first ? X_EMBED_NORM : X_NORM;
       qa.gain = c->W<void>(lw.attn_norm);
       qa.embed = c->W<void>(o.embed);
       qa.tok = tok;
       qa.vocab = o.V;
       // the pass's argmax slots are cleared by its first kernel
-      if (j == l_begin && zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = vec ? 1 : M; }
-    } else if (j > l_begin) {
-      split_norm_consume(c, qa);  // prepared by the previous layer's down projection
+      if (zero_slot) { qa.zero_keys = zero_slot; qa.n_zero_keys = 1; }
     } else {
       NormArgs na{};
       na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
@@ -484,7 +489,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     oa.n_groups = o.d / 16; oa.KT = k_tiles(dt, o.qd); oa.K = o.qd;
     oa.x_mode = X_PLAIN; oa.x = c->S<void>(o.attn_out); oa.ldx = o.qd;
     oa.epi = EPI_RESID;
-    if (!vec) split_norm_produce(c, oa, c->W<void>(lw.ffn_norm));
+    split_norm_produce(c, oa, c->W<void>(lw.ffn_norm));
     LAUNCH_LINEAR(vec, oa, dt);
 
     // feed-forward block
@@ -494,11 +499,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     ga.w = c->W<uint8_t>(lw.wgu);
     ga.n_groups = 2 * o.F / 16; ga.KT = k_tiles(dt, o.d); ga.K = o.d;
     ga.epi = EPI_SWIGLU; ga.act = c->S<void>(o.act); ga.ld_act = o.Fp;
-    if (vec) {
-      ga.x_mode = X_NORM; ga.gain = c->W<void>(lw.ffn_norm);
-    } else {
-      split_norm_consume(c, ga);
-    }
+    split_norm_consume(c, ga);  // prepared by the output projection
     LAUNCH_LINEAR(vec, ga, dt);
 
     LinearArgs da = base_linear(c);
@@ -508,10 +509,10 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     da.n_groups = o.d / 16; da.KT = k_tiles(dt, o.F); da.K = o.F;
     da.x_mode = X_PLAIN; da.x = c->S<void>(o.act); da.ldx = o.Fp;
     da.epi = EPI_RESID;
-    // the next norm: the next layer's attention norm, or the final norm when
-    // the pass ends at the last layer (the head follows)
-    if (!vec && j + 1 < l_end) split_norm_produce(c, da, c->W<void>(o.lay[j + 1].attn_norm));
-    else if (!vec && l_end == o.L) split_norm_produce(c, da, c->W<void>(o.final_norm));
+    // the next norm: the next layer's attention norm, or the final norm at
+    // the end of a pass that a head follows (one-row passes end at an exit)
+    if (j + 1 < l_end) split_norm_produce(c, da, c->W<void>(o.lay[j + 1].attn_norm));
+    else if (vec || l_end == o.L) split_norm_produce(c, da, c->W<void>(o.final_norm));
     LAUNCH_LINEAR(vec, da, dt);
 
     if (qnet_after == j + 1 && o.H > 0) {
@@ -537,9 +538,12 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 }
 
 // Shared final RMSNorm + LM head + argmax for rows [0, M) into keys[0..M).
-// split: a multi-row pass through the last layer prepared the final norm.
+// split: a multi-row pass through the last layer prepared the final norm
+// (one-row heads use the split when the last one-row pass ended on their row).
 int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s, int vec_row = 0,
              bool split = false) {
+  if (vec) split = c->split_row == vec_row;
+  else c->split_row = -1;
   const Layout& o = c->lo;
   LinearArgs ha = base_linear(c);
   ha.M = M;
@@ -548,10 +552,10 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
   ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
   ha.logits = logits; ha.ld_logits = o.V;
-  if (vec) {
-    ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
-  } else if (split) {
+  if (split) {
     split_norm_consume(c, ha);
+  } else if (vec) {
+    ha.x_mode = X_NORM; ha.gain = c->W<void>(o.final_norm);
   } else {
     NormArgs na{};
     na.M = M; na.d = o.d; na.ldh = o.d; na.ldx = o.d;
