@@ -38,7 +38,7 @@ struct Layout {
   size_t embed, final_norm, head, qw1, qb1, qw2, qb2, ew1, eb1, ew2, eb2, wbytes;
   int He;  // exit-policy Q-network hidden width (0: none)
   // workspace offsets
-  size_t h, xn, ss, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, qaction, seq_len, btab, prompt,
+  size_t h, xn, ss, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, seq_len, btab, prompt,
       record, rope, unif, dstats, trace, trace_state, pol_out, wsbytes;
   size_t kvbytes, kv_half;
 };
@@ -122,7 +122,6 @@ Layout make_layout(const lede_config* c) {
   o.qs = take((size_t)o.d * 4);
   o.qhid = take((size_t)(o.H ? o.H : 1) * 4);
   o.qv = take((size_t)(o.A ? o.A : 1) * 4);
-  o.qaction = take(16 * 4);
   o.seq_len = take(4);
   o.btab = take((size_t)o.max_pages_seq * 4);
   o.prompt = take((size_t)o.max_ctx * 4);
@@ -165,6 +164,7 @@ struct lede_ctx {
   int use_graphs = 0, debug = 0;
   int verify_reuse = 0;  // verify from the exit layer on the draft passes' hidden states and KV
   int split_row = -1;    // the one-row residual row whose final-norm split the last pass prepared
+  std::vector<int32_t> table_dev;  // the block table as the device holds it (uploads are skipped when equal)
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
@@ -333,10 +333,18 @@ void truncate_pages(lede_ctx* c, int new_len) {
   if ((int)c->table.size() > keep) c->table.resize(keep);
 }
 
+// Upload the host table if the device's differs (the acceptance kernel
+// truncates the device table itself; commit_host mirrors that).
 int upload_table(lede_ctx* c, hipStream_t s) {
   const int n = c->lo.max_pages_seq;
-  for (int j = 0; j < n; ++j) c->table_h[j] = j < (int)c->table.size() ? c->table[j] : -1;
+  bool same = (int)c->table_dev.size() == n;
+  for (int j = 0; j < n; ++j) {
+    c->table_h[j] = j < (int)c->table.size() ? c->table[j] : -1;
+    same = same && c->table_dev[j] == c->table_h[j];
+  }
+  if (same) return LEDE_OK;
   HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.btab), c->table_h, n * 4, hipMemcpyHostToDevice, s));
+  c->table_dev.assign(c->table_h, c->table_h + n);
   return LEDE_OK;
 }
 
@@ -530,7 +538,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       QnetOutArgs qo{};
       qo.hid = c->S<float>(o.qhid); qo.H = o.H;
       qo.w2 = c->W<float>(o.qw2); qo.b2 = c->W<float>(o.qb2); qo.A = o.A;
-      qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.qaction);
+      qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.record) + 48;
       LAUNCH(LEDE_K_QNET, (double)o.A * (o.H + 2) * 4, launch_qnet_out(qo, s));
     }
   }
@@ -690,8 +698,10 @@ int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
   return LEDE_OK;
 }
 
+// The acceptance record, and the Q-network's action and value (slots 48..49,
+// written there by the Q-network's output kernel), in one read-back.
 int read_record(lede_ctx* c, hipStream_t s) {
-  HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 48 * 4, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 50 * 4, hipMemcpyDeviceToHost, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
   return LEDE_OK;
 }
@@ -702,6 +712,8 @@ void commit_host(lede_ctx* c) {
   c->seq_len = c->record_h[2];
   c->pending = c->record_h[3];
   truncate_pages(c, c->seq_len);
+  // the acceptance kernel cleared the device entries past the kept pages
+  for (size_t j = c->table.size(); j < c->table_dev.size(); ++j) c->table_dev[j] = -1;
   c->drafted_k = -1;
 }
 
@@ -766,6 +778,7 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
     lede_destroy(c);
     return LEDE_E_HIP;
   }
+  c->table_dev = bt;
   *out = c;
   return LEDE_OK;
 }
@@ -1035,7 +1048,7 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       uint64_t* dk = c->S<uint64_t>(o.dkeys);
       rc = run_layers(c, 1, true, TokenSrc{nullptr, dk}, 0, 0, l_min, l_min, dk + 1, s);
       if (rc) return rc;
-      HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
+      HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.record) + 48, 2 * 4, hipMemcpyDeviceToHost, s));
       HIP_CHECK(c, hipStreamSynchronize(s));
       const int a = c->record_h[48];
       if (a < 0 || a >= o.A) return fail(c, LEDE_E_HIP, "Q-network action %d out of range", a);
@@ -1079,7 +1092,6 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
     if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
   }
 verified:
-  if (ran_q) HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.qaction), 2 * 4, hipMemcpyDeviceToHost, s));
   rc = read_record(c, s);
   if (rc) return rc;
   commit_host(c);
