@@ -41,11 +41,18 @@ __global__ void k_accept(AcceptArgs a) {
 __global__ __launch_bounds__(SB) void k_sample(SampleArgs a) {
   __shared__ float red[SW];
   __shared__ int ired[SW];
-  const float2 st = row_stats(a.logits, a.vocab, a.inv_t, red);
-  const float m = st.x, it = a.inv_t;
   const float u = a.u ? a.u[a.u_index] : a.u_imm;
-  const int tok = block_draw([&](float x, float) { return expf((x - m) * it); }, a.logits, nullptr, a.vocab, u,
-                             red, ired);
+  const float it = a.inv_t;
+  float2 st;
+  int tok;
+  if (a.gstats) {  // from the head's group statistics: no pass over the row
+    st = group_row_stats(a.gstats, a.n_groups, it, red);
+    tok = group_draw(a.gstats, a.logits, a.n_groups, st.x, it, u, red, ired);
+  } else {
+    st = row_stats(a.logits, a.vocab, it, red);
+    const float m = st.x;
+    tok = block_draw([&](float x, float) { return expf((x - m) * it); }, a.logits, nullptr, a.vocab, u, red, ired);
+  }
   if (threadIdx.x == 0) {
     key_store_token(a.key_out, 0, tok);
     if (a.stats_out) {
@@ -65,7 +72,8 @@ __global__ __launch_bounds__(SB) void k_accept_sampled(SampledAcceptArgs a) {
   const int k = a.acc.k, V = a.vocab;
   const float it = a.inv_t;
   for (int j = 0; j <= k; ++j) {
-    const float2 st = row_stats(a.vlogits + (size_t)j * V, V, it, red);
+    const float2 st = a.vgstats ? group_row_stats(a.vgstats + (size_t)j * a.n_groups, a.n_groups, it, red)
+                                : row_stats(a.vlogits + (size_t)j * V, V, it, red);
     if (threadIdx.x == 0) {
       vst[2 * j] = st.x;
       vst[2 * j + 1] = st.y;
@@ -97,6 +105,8 @@ __global__ __launch_bounds__(SB) void k_accept_sampled(SampledAcceptArgs a) {
     // rounding can leave no positive residual weight; the target row is
     // then the residual's only possible limit
     if (y < 0) y = block_draw([&](float x, float) { return expf((x - mp) * it); }, zp, nullptr, V, ur, red, ired);
+  } else if (a.vgstats) {
+    y = group_draw(a.vgstats + (size_t)acc * a.n_groups, zp, a.n_groups, mp, it, ur, red, ired);
   } else {
     y = block_draw([&](float x, float) { return expf((x - mp) * it); }, zp, nullptr, V, ur, red, ired);
   }

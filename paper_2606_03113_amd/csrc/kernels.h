@@ -61,6 +61,8 @@ struct SampleArgs {
   float u_imm;
   uint64_t* key_out;             // argmax-style key of the drawn token
   float* stats_out;              // (max, sum) of the row
+  const float2* gstats;          // optional: the row's 16-token group statistics (vocab = 16 n_groups)
+  int n_groups;
 };
 struct SampledAcceptArgs {
   AcceptArgs acc;                // keys, k, commit targets
@@ -69,6 +71,8 @@ struct SampledAcceptArgs {
   const float* vlogits;          // [k+1][vocab]
   int vocab; float inv_t;
   const float* u;                // the step's uniforms
+  const float2* vgstats;         // optional: [k+1][n_groups] group statistics of the verify rows
+  int n_groups;
 };
 
 // The paper's exit policy: state features of a next-token distribution and

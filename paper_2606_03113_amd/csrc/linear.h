@@ -121,6 +121,9 @@ struct LinearArgs {
   void* act; int ld_act;
   // EPI_ARGMAX
   uint64_t* keys; float* logits; int ld_logits; int vocab;
+  // optional, with logits: per 16-token group g of row m, (max z, sum of
+  // exp((z - max) * inv_t)) at gstats[m * ld_gstats + g]
+  float2* gstats; int ld_gstats; float inv_t;
   // RMSNorm split over two kernels.  A residual producer (EPI_RESID) with
   // ss_out also stores xg[m][n] = h[m][n] * xg_gain[n] in the model dtype and,
   // per 16-column group g of its n_groups, the sum of squares of its columns

@@ -77,7 +77,7 @@ __device__ __forceinline__ QkvPre qkv_fetch(const LinearArgs& a, int g, int c) {
   return p;
 }
 
-template <int DT>
+template <int DT, bool GS>
 __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)[17], uint64_t& best, int qkv_c,
                                          const QkvPre& pre) {
   const int tid = threadIdx.x;
@@ -171,6 +171,14 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
             const uint64_t key = argmax_key(ct[nn][tid], rr);
             best = key > best ? key : best;
           }
+        }
+        if (GS) {  // the group's sampling statistics, in token order
+          float gm = -INFINITY, gs = 0.f;
+          for (int nn = 0; nn < 16; ++nn)
+            if (g * 16 + nn < a.vocab) gm = fmaxf(gm, ct[nn][tid]);
+          for (int nn = 0; nn < 16; ++nn)
+            if (g * 16 + nn < a.vocab && gm > -INFINITY) gs += expf((ct[nn][tid] - gm) * a.inv_t);
+          a.gstats[(size_t)tid * a.ld_gstats + g] = make_float2(gm, gs);
         }
       }
       break;
@@ -310,9 +318,10 @@ __device__ void copy_row_stage(const CopyRow<NW>& cr, int pad, uint8_t* lds) {
 //                   global-to-LDS loads issued before its weights) into a
 //                   region of its own, [row m][tile j][64 bytes], so that it
 //                   waits for its own loads only.
-// Six waves per SIMD (at most 80 VGPRs) keeps three blocks per CU.
-template <int DT, int XS>
-__global__ __launch_bounds__(LIN_WAVES * 64) __attribute__((amdgpu_waves_per_eu(6))) void k_linear(LinearArgs a) {
+// GS: the argmax epilogue also writes the sampling group statistics (a
+// separate kernel, so that the others carry none of its registers).
+template <int DT, int XS, bool GS>
+__device__ __forceinline__ void linear_main(const LinearArgs& a) {
   typedef Tile<DT> TL;
   constexpr int NW = LIN_WAVES, U = 4;  // tiles per wave per batch
   constexpr bool MFMA = XS == XS_MFMA || XS == XS_MFMA_LDS;
@@ -493,7 +502,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) __attribute__((amdgpu_waves_per_eu(
       }
     }
     __syncthreads();
-    if (tid < 256) epilogue<DT>(a, g, ct, best, qkv_c, qpre);
+    if (tid < 256) epilogue<DT, GS>(a, g, ct, best, qkv_c, qpre);
     __syncthreads();
     if (a.epi == EPI_RESID && a.ss_out && tid < 16) {
       float s = 0.f;
@@ -504,6 +513,17 @@ __global__ __launch_bounds__(LIN_WAVES * 64) __attribute__((amdgpu_waves_per_eu(
   }
   if (a.epi == EPI_ARGMAX && tid < 16 && tid < a.M && best)
     atomicMax((unsigned long long*)&a.keys[(blockIdx.x % KEY_SLOTS) * KEY_PITCH + tid], (unsigned long long)best);
+}
+
+// Six waves per SIMD (at most 80 VGPRs) keeps three blocks per CU.
+template <int DT, int XS>
+__global__ __launch_bounds__(LIN_WAVES * 64) __attribute__((amdgpu_waves_per_eu(6))) void k_linear(LinearArgs a) {
+  linear_main<DT, XS, false>(a);
+}
+// The heads of sampled passes (2 blocks per CU): no occupancy target.
+template <int DT, int XS>
+__global__ __launch_bounds__(LIN_WAVES * 64) void k_linear_gs(LinearArgs a) {
+  linear_main<DT, XS, true>(a);
 }
 
 // ---- launchers ----------------------------------------------------------------
@@ -543,10 +563,16 @@ size_t linear_lds_bytes(int dtype, bool mfma, int x_mode, int K, int M) {
 template <int DT, int XS>
 static void launch_linear_t(const LinearArgs& a, int grid, size_t lds, hipStream_t s, hipEvent_t e0,
                             hipEvent_t e1) {
-  if (e0)
+  if (a.gstats) {
+    if (e0)
+      hipExtLaunchKernelGGL((k_linear_gs<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), (uint32_t)lds, s, e0, e1, 0, a);
+    else
+      hipLaunchKernelGGL((k_linear_gs<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), lds, s, a);
+  } else if (e0) {
     hipExtLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), (uint32_t)lds, s, e0, e1, 0, a);
-  else
+  } else {
     hipLaunchKernelGGL((k_linear<DT, XS>), dim3(grid), dim3(LIN_WAVES * 64), lds, s, a);
+  }
 }
 
 hipError_t launch_linear(int dtype, bool mfma, const LinearArgs& a, int grid, hipStream_t s, hipEvent_t e0,

@@ -146,4 +146,74 @@ __device__ inline float2 row_stats(const float* z, int V, float inv_t, float* re
   return make_float2(m, total);
 }
 
+// ---- the same from per-group statistics --------------------------------------
+// A row of V = 16 G tokens summarised by its groups' (max m_g, sum of
+// exp((z - m_g) * inv_t)): thread t owns the contiguous groups
+// [t D, (t+1) D) (D = ceil(G / SB)), and every sum runs in group order within
+// a thread and in thread order across the block.
+
+__device__ __forceinline__ int group_chunk(int G) { return (G + SB - 1) / SB; }
+
+// Weight of group g relative to the row maximum mx: sum over its tokens of
+// exp((z - mx) * inv_t).
+__device__ __forceinline__ float group_weight(float2 st, float mx, float inv_t) {
+  return st.x > -INFINITY ? st.y * expf((st.x - mx) * inv_t) : 0.f;
+}
+
+// (max, sum of exp((z - max) * inv_t)) of the row from its group statistics.
+__device__ inline float2 group_row_stats(const float2* gs, int G, float inv_t, float* red) {
+  const int D = group_chunk(G), g0 = threadIdx.x * D, g1 = min(G, g0 + D);
+  float m = -INFINITY;
+  for (int g = g0; g < g1; ++g) m = fmaxf(m, gs[g].x);
+  m = block_max_f(m, red);
+  float s = 0.f;
+  for (int g = g0; g < g1; ++g) s += group_weight(gs[g], m, inv_t);
+  float total;
+  (void)block_excl_scan(s, red, total);
+  __syncthreads();
+  return make_float2(m, total);
+}
+
+// Inverse-CDF draw at temperature 1 / inv_t from the row z with group
+// statistics gs and row maximum mx: the group whose running weight crosses
+// u * total, then the token within it whose running weight does (else, by
+// rounding, the group's last token of positive weight).  -1 when the total
+// weight is 0.
+__device__ int group_draw(const float2* gs, const float* z, int G, float mx, float inv_t, float u, float* red,
+                          int* ired) {
+  const int D = group_chunk(G), g0 = threadIdx.x * D, g1 = min(G, g0 + D);
+  float s = 0.f;
+  for (int g = g0; g < g1; ++g) s += group_weight(gs[g], mx, inv_t);
+  float total;
+  const float pre = block_excl_scan(s, red, total);
+  const float thr = u * total;
+  const int owner = block_max_i((s > 0.f && pre <= thr) ? (int)threadIdx.x : -1, ired);
+  __shared__ int tok;
+  if ((int)threadIdx.x == owner) {
+    float acc = pre;  // running weight before group g
+    int gsel = -1, glast = -1;
+    for (int g = g0; g < g1; ++g) {
+      const float w = group_weight(gs[g], mx, inv_t);
+      if (w > 0.f) glast = g;
+      if (w > 0.f && acc + w > thr) {
+        gsel = g;
+        break;
+      }
+      acc += w;
+    }
+    const int gg = gsel >= 0 ? gsel : glast;  // glast: rounding left the crossing past the chunk
+    int hit = -1, last = -1;
+    for (int j = 0; j < 16; ++j) {
+      const float w = expf((z[gg * 16 + j] - mx) * inv_t);
+      if (w > 0.f) last = gg * 16 + j;
+      acc += w;
+      if (gsel >= 0 && hit < 0 && acc > thr) hit = gg * 16 + j;
+    }
+    tok = hit >= 0 ? hit : last;
+  }
+  if (threadIdx.x == 0 && owner < 0) tok = -1;
+  __syncthreads();
+  return tok;
+}
+
 }  // namespace lede

@@ -38,7 +38,7 @@ struct Layout {
   size_t embed, final_norm, head, qw1, qb1, qw2, qb2, ew1, eb1, ew2, eb2, wbytes;
   int He;  // exit-policy Q-network hidden width (0: none)
   // workspace offsets
-  size_t h, xn, ss, q, attn_out, act, part, logits, dkeys, vkeys, qs, qhid, qv, seq_len, btab, prompt,
+  size_t h, xn, ss, q, attn_out, act, part, logits, gstats, dkeys, vkeys, qs, qhid, qv, seq_len, btab, prompt,
       record, rope, unif, dstats, trace, trace_state, pol_out, wsbytes;
   size_t kvbytes, kv_half;
 };
@@ -117,6 +117,7 @@ Layout make_layout(const lede_config* c) {
   o.act = take((size_t)MROWS * o.Fp * o.es);
   o.part = take((size_t)MROWS * o.nq * o.max_chunks * (o.hd + 2) * 4);
   o.logits = take((size_t)2 * MROWS * o.V * 4);
+  o.gstats = take((size_t)2 * MROWS * (o.V / 16) * 8);  // group statistics of sampled logits rows
   o.dkeys = take(KEY_WORDS * 8);
   o.vkeys = take(KEY_WORDS * 8);
   o.qs = take((size_t)o.d * 4);
@@ -305,7 +306,7 @@ double linear_bytes(const LinearArgs& a, int dt) {
     case EPI_RESID: y = 2 * M * N * 4; break;
     case EPI_QKV: y = M * N * 4; break;
     case EPI_SWIGLU: y = M * N / 2 * es; break;
-    case EPI_ARGMAX: y = M * 8 + (a.logits ? M * N * 4 : 0); break;
+    case EPI_ARGMAX: y = M * 8 + (a.logits ? M * N * 4 : 0) + (a.gstats ? M * N / 16 * 8 : 0); break;
     default: y = M * N * 4;
   }
   if (a.ss_out) y += M * N * es + N * es + N / 16 * M * 4;  // h * gain, the gain, the partial sums
@@ -548,8 +549,9 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
 // Shared final RMSNorm + LM head + argmax for rows [0, M) into keys[0..M).
 // split: a multi-row pass through the last layer prepared the final norm
 // (one-row heads use the split when the last one-row pass ended on their row).
+// gstats (with logits): also the rows' 16-token group statistics at inv_t.
 int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStream_t s, int vec_row = 0,
-             bool split = false) {
+             bool split = false, float2* gstats = nullptr, float inv_t = 0.f) {
   if (vec) split = c->split_row == vec_row;
   else c->split_row = -1;
   const Layout& o = c->lo;
@@ -560,6 +562,7 @@ int run_head(lede_ctx* c, int M, bool vec, uint64_t* keys, float* logits, hipStr
   ha.n_groups = o.V / 16; ha.KT = k_tiles(o.dt, o.d); ha.K = o.d;
   ha.epi = EPI_ARGMAX; ha.keys = keys; ha.vocab = o.V;
   ha.logits = logits; ha.ld_logits = o.V;
+  if (logits && gstats) { ha.gstats = gstats; ha.ld_gstats = o.V / 16; ha.inv_t = inv_t; }
   if (split) {
     split_norm_consume(c, ha);
   } else if (vec) {
@@ -584,6 +587,8 @@ float* draft_logits(lede_ctx* c, int i, bool always = false) {
 float* verify_logits(lede_ctx* c, bool always = false) {
   return (c->debug || always) ? c->S<float>(c->lo.logits) : nullptr;
 }
+// Group statistics of logits row r (same row order as the logits).
+float2* logits_gstats(lede_ctx* c, int r) { return c->S<float2>(c->lo.gstats) + (size_t)r * (c->lo.V / 16); }
 
 // Draft passes i = i0..k (1-based): token i-1 -> layers [0, l) -> head -> key i.
 // qnet_after applies to pass 1 only.  inv_t > 0: draft i is drawn from
@@ -597,14 +602,16 @@ int launch_drafts(lede_ctx* c, int l, int i0, int k, int qnet_after, int pass1_b
     const int begin = i == 1 ? pass1_begin : 0;
     int rc = run_layers(c, 1, true, tok, i - 1, begin, l, i == 1 ? qnet_after : 0, dk + i, s, i - 1);
     if (rc) return rc;
-    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1, sampled), s, i - 1);
+    rc = run_head(c, 1, true, dk + i, draft_logits(c, i - 1, sampled), s, i - 1, false,
+                  sampled ? logits_gstats(c, MROWS + i - 1) : nullptr, inv_t);
     if (rc) return rc;
     if (sampled) {
       SampleArgs sa{};
       sa.logits = draft_logits(c, i - 1, true); sa.vocab = c->lo.V; sa.inv_t = inv_t;
       sa.u = c->S<float>(c->lo.unif); sa.u_index = i - 1;
       sa.key_out = dk + i; sa.stats_out = c->S<float>(c->lo.dstats) + 2 * (i - 1);
-      LAUNCH(LEDE_K_ACCEPT, (double)c->lo.V * 4, launch_sample(sa, s));
+      sa.gstats = logits_gstats(c, MROWS + i - 1); sa.n_groups = c->lo.V / 16;
+      LAUNCH(LEDE_K_ACCEPT, (double)c->lo.V / 16 * 8 + 64, launch_sample(sa, s));
     }
   }
   c->last_draft_rows = k;
@@ -646,7 +653,8 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from
   } else if ((rc = run_layers(c, k + 1, false, tok, 0, from_layer, c->lo.L, 0, vk, s))) {
     return rc;
   }
-  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s, 0, from_layer < c->lo.L);
+  rc = run_head(c, k + 1, false, vk, verify_logits(c, sampled || trace), s, 0, from_layer < c->lo.L,
+                sampled ? logits_gstats(c, 0) : nullptr, inv_t);
   if (rc) return rc;
   AcceptArgs aa{};
   aa.dkeys = dk; aa.vkeys = vk; aa.k = k;
@@ -661,6 +669,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from
     sa.vlogits = verify_logits(c, true);
     sa.vocab = c->lo.V; sa.inv_t = inv_t;
     sa.u = c->S<float>(c->lo.unif);
+    sa.vgstats = logits_gstats(c, 0); sa.n_groups = c->lo.V / 16;
     LAUNCH(LEDE_K_ACCEPT, (double)(2 * k + 1) * c->lo.V * 4, launch_accept_sampled(sa, s));
   } else {
     LAUNCH(LEDE_K_ACCEPT, 256.0, launch_accept(aa, s));
