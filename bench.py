@@ -107,7 +107,21 @@ def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": toks / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": "%d SSD steps (l=%d, k=%d) of %s from KV length %d (prompt KV filled with synthetic "
-                      "bf16 values, no oracle prefill); %.1f s" % (steps, l, k, wl.name, P, el)}
+                      "bf16 values, no oracle prefill); %.1f s" % (steps, l, k, wl.name, P, el),
+            "host": "%s; %d logical CPUs visible; OMP_NUM_THREADS=%s" % (
+                host_cpu_model(), os.cpu_count() or 0, os.environ.get("OMP_NUM_THREADS", "unset"))}
+
+
+def host_cpu_model():
+    """The host CPU's model name (Linux /proc/cpuinfo), or 'unknown'."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def dqn_leg(torch, li, n_updates=2000, H=16, B=32):
