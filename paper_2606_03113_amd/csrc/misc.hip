@@ -6,25 +6,56 @@ namespace lede {
 
 // ---- Q-network output layer + argmax ----------------------------------------
 
-// One wavefront per action: q[j] = sum_i W2[j][i] hid[i] + b2[j]; argmax with
-// the lowest index on ties.
-__global__ __launch_bounds__(256) void k_qnet_out(QnetOutArgs a) {
-  __shared__ unsigned long long best[4];
+// q[j] = sum_i W2[j][i] hid[i] + b2[j] for every action j, with 16
+// wavefronts taking actions j = w, w + 16, ...; argmax with the lowest index
+// on ties.  Lane l sums i = l, l + 64, ... in order.  Up to QNA actions per
+// wavefront and QNC 64-wide chunks of the hidden layer, every load is issued
+// before the first sum (one memory round trip); larger networks loop.
+constexpr int QNW = 16, QNA = 4, QNC = 4;
+__global__ __launch_bounds__(QNW * 64) void k_qnet_out(QnetOutArgs a) {
+  __shared__ unsigned long long best[QNW];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   uint64_t b = 0;
-  for (int j = wave; j < a.A; j += 4) {
-    float s = 0.f;
-    for (int i = lane; i < a.H; i += 64) s = fmaf(a.w2[(size_t)j * a.H + i], a.hid[i], s);
-    s = wave_sum(s) + a.b2[j];
-    if (lane == 0) a.qv[j] = s;
-    const uint64_t key = argmax_key(s, j);
-    b = key > b ? key : b;
+  if (a.A <= QNW * QNA && a.H <= 64 * QNC) {
+    float hv[QNC], wv[QNA][QNC], bv[QNA];
+#pragma unroll
+    for (int c = 0; c < QNC; ++c) hv[c] = lane + 64 * c < a.H ? a.hid[lane + 64 * c] : 0.f;
+#pragma unroll
+    for (int q = 0; q < QNA; ++q) {
+      const int j = wave + QNW * q;
+      bv[q] = j < a.A ? a.b2[j] : 0.f;
+#pragma unroll
+      for (int c = 0; c < QNC; ++c)
+        wv[q][c] = (j < a.A && lane + 64 * c < a.H) ? a.w2[(size_t)j * a.H + lane + 64 * c] : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < QNA; ++q) {
+      const int j = wave + QNW * q;
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < QNC; ++c) s = fmaf(wv[q][c], hv[c], s);
+      s = wave_sum(s) + bv[q];
+      if (j < a.A) {
+        if (lane == 0) a.qv[j] = s;
+        const uint64_t key = argmax_key(s, j);
+        b = key > b ? key : b;
+      }
+    }
+  } else {
+    for (int j = wave; j < a.A; j += QNW) {
+      float s = 0.f;
+      for (int i = lane; i < a.H; i += 64) s = fmaf(a.w2[(size_t)j * a.H + i], a.hid[i], s);
+      s = wave_sum(s) + a.b2[j];
+      if (lane == 0) a.qv[j] = s;
+      const uint64_t key = argmax_key(s, j);
+      b = key > b ? key : b;
+    }
   }
   if (lane == 0) best[wave] = b;
   __syncthreads();
   if (tid == 0) {
     uint64_t m = best[0];
-    for (int w = 1; w < 4; ++w) m = best[w] > m ? best[w] : m;
+    for (int w = 1; w < QNW; ++w) m = best[w] > m ? best[w] : m;
     const int idx = (int)(0xFFFFFFFFu - (uint32_t)(m & 0xFFFFFFFFull));
     a.action[0] = idx;
     uint32_t u = (uint32_t)(m >> 32);
@@ -101,7 +132,7 @@ __global__ __launch_bounds__(LIN_WAVES * 64) void k_read_groups(const uint8_t* s
 // ---- launchers ----------------------------------------------------------------
 
 hipError_t launch_qnet_out(const QnetOutArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_qnet_out, dim3(1), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(k_qnet_out, dim3(1), dim3(QNW * 64), 0, s, a);
   return hipGetLastError();
 }
 
