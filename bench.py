@@ -187,6 +187,9 @@ def main():
     ap.add_argument("--verify-reuse", action="store_true",
                     help="verify from the exit layer on the draft passes' hidden states and KV")
     ap.add_argument("--graphs", type=int, default=0)
+    ap.add_argument("--in-flight", type=int, default=1,
+                    help="forced greedy eager steps: how many are queued on the stream before the oldest "
+                         "record is read back (1: one synchronous lede_step at a time)")
     ap.add_argument("--policy", choices=["fixed", "paper"], default="fixed",
                     help="paper: the paper's exit policy (seeded random exit Q-network) chooses l* and k per step")
     ap.add_argument("--temperature", type=float, default=0.0,
@@ -266,12 +269,41 @@ def main():
         produced.extend(rec.emitted)
         return rec
 
+    from paper_2606_03113_amd.lede import MAX_IN_FLIGHT
+    if not 1 <= args.in_flight <= MAX_IN_FLIGHT:
+        sys.exit("--in-flight must be in 1..%d" % MAX_IN_FLIGHT)
+    pipelined = (args.in_flight > 1 and not paper and args.temperature == 0 and not args.graphs
+                 and not args.verify_reuse)
+
+    def run_steps(n):
+        """n steps; pipelined, each step is queued while up to in_flight - 1 earlier
+        ones still run, and n_remaining is the fewest tokens that can be left."""
+        if not pipelined:
+            return [step() for _ in range(n)]
+        rs, queued = [], []  # queued: the k_eff bound of each step in flight
+
+        def collect():
+            r = eng.lede_step_collect()
+            queued.pop(0)
+            produced.extend(r.emitted)
+            rs.append(r)
+
+        for _ in range(n):
+            if len(queued) == args.in_flight:
+                collect()
+            left = max(1, wl.n_gen - len(produced) - sum(q + 1 for q in queued))
+            eng.lede_step_submit((l, k), n_remaining=left, log_qnet=log_q)
+            queued.append(min(k, left - 1))
+            n_steps[0] += 1
+        while queued:
+            collect()
+        return rs
+
     if args.graphs and args.temperature > 0:
         sys.exit("sampled steps are not captured in graphs")
     if args.warmup + args.steps >= wl.n_gen - 1:
         sys.exit("warmup + steps must stay below the %d generated tokens" % wl.n_gen)
-    for _ in range(args.warmup):
-        step()
+    run_steps(args.warmup)
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -279,8 +311,7 @@ def main():
     recs = []
     w0 = time.perf_counter()
     e0.record(stream)
-    for _ in range(args.steps):
-        recs.append(step())
+    recs = run_steps(args.steps)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -448,6 +479,7 @@ def main():
                                 "static exit l=%d, draft k=%d, Q-network logged" % (l, k)),
                    "batch": 1, "prompt_len": wl.prompt_len, "exit_layer": l, "draft_len": k,
                    "graphs": bool(args.graphs), "verify_reuse": bool(args.verify_reuse),
+                   "steps_in_flight": args.in_flight if pipelined else 1,
                    "acceptance": ("speculative sampling, T=%g" % args.temperature if args.temperature > 0
                                   else "greedy"),
                    "policy": "paper exit policy (random exit Q-network)" if paper else "fixed"},

@@ -205,6 +205,30 @@ int lede_verify(lede_ctx* ctx, void* stream, int32_t* accepted, int32_t* tokens,
 int lede_step(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
               void* stream, lede_step_record* rec);
 
+/* Pipelined steps (the same step as lede_step with a forced action, greedy
+ * acceptance): lede_step_submit enqueues the whole step on `stream` (drafts,
+ * verify, acceptance, and the record's read-back into a host slot) and
+ * returns without waiting; lede_step_collect waits for the oldest submitted
+ * step and fills *rec exactly as lede_step would have.  The device holds the
+ * committed length, the pending token and the page table, so step n+1 needs
+ * nothing from step n's record and can be queued behind it: the host's work
+ * between steps overlaps the GPU's.  Pages are allocated for the longest
+ * acceptance of every step in flight and returned at collection, so a
+ * submit can fail with LEDE_E_CTX_OVERFLOW or LEDE_E_KV_FULL where a
+ * synchronous step would not (collect and retry, or step synchronously).
+ * k is clamped to n_remaining - 1 with the n_remaining given at submission.
+ * Errors: LEDE_E_ARG for a null ctx or action, n_remaining < 1, or l or k
+ * out of range; LEDE_E_HIP when a launch or copy fails.  At
+ * most LEDE_MAX_IN_FLIGHT steps may be outstanding (LEDE_E_STATE beyond, or
+ * when collecting with none); while any is, every other decoding call
+ * returns LEDE_E_STATE.  Submit and collect must use the same stream.
+ * Graph replay, profiling, verify reuse and sampling are not pipelined
+ * (LEDE_E_STATE when enabled). */
+#define LEDE_MAX_IN_FLIGHT 2
+int lede_step_submit(lede_ctx* ctx, const lede_action* action, int32_t log_qnet, int32_t n_remaining,
+                     void* stream);
+int lede_step_collect(lede_ctx* ctx, void* stream, lede_step_record* rec);
+
 /* ---- speculative sampling (Section 4.1: sampling at temperature T, e.g.
  * 0.6, with speculative-sampling acceptance) -------------------------------
  * A step as lede_step, except that

@@ -166,6 +166,18 @@ struct lede_ctx {
   int verify_reuse = 0;  // verify from the exit layer on the draft passes' hidden states and KV
   int split_row = -1;    // the one-row residual row whose final-norm split the last pass prepared
   std::vector<int32_t> table_dev;  // the block table as the device holds it (uploads are skipped when equal)
+  // pipelined steps (lede_step_submit / lede_step_collect), oldest first
+  struct InFlight {
+    int l, k_req, k_eff, slot;
+    bool ran_q;
+  };
+  std::deque<InFlight> inflight;
+  int32_t* rec_slots_h = nullptr;          // pinned [LEDE_MAX_IN_FLIGHT][RECORD_INTS]
+  hipEvent_t rec_ev[LEDE_MAX_IN_FLIGHT] = {};
+  hipEvent_t wait_ev = nullptr;            // the read-backs of a synchronous step wait on it
+  int next_slot = 0;
+  int seq_ub = 0;                          // committed length after every step in flight, at most
+  void* pipe_stream = nullptr;
   // captured draft + verify launches of a forced step, keyed by (l, k_eff, Q-net layer)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
@@ -328,6 +340,10 @@ int ensure_pages(lede_ctx* c, int n_positions) {
   return LEDE_OK;
 }
 
+// Ints between the pinned table staging buffers (the synchronous one, then
+// one per pipelined slot).
+size_t table_pitch(const Layout& o) { return ((size_t)o.max_pages_seq + 63) / 64 * 64; }
+
 void truncate_pages(lede_ctx* c, int new_len) {
   const int keep = (new_len + PAGE - 1) / PAGE;
   for (int j = (int)c->table.size() - 1; j >= keep; --j) c->free_list.push_front(c->table[j]);
@@ -335,17 +351,30 @@ void truncate_pages(lede_ctx* c, int new_len) {
 }
 
 // Upload the host table if the device's differs (the acceptance kernel
-// truncates the device table itself; commit_host mirrors that).
-int upload_table(lede_ctx* c, hipStream_t s) {
+// truncates the device table itself; commit_host mirrors that, and a
+// pipelined step marks the entries it may clear as unknown).  `stage` is the
+// pinned buffer the copy reads: a pipelined step passes its slot's, which no
+// later submit overwrites before the copy has run.
+int upload_table(lede_ctx* c, hipStream_t s, int32_t* stage = nullptr) {
   const int n = c->lo.max_pages_seq;
+  int32_t* t = stage ? stage : c->table_h;
   bool same = (int)c->table_dev.size() == n;
   for (int j = 0; j < n; ++j) {
-    c->table_h[j] = j < (int)c->table.size() ? c->table[j] : -1;
-    same = same && c->table_dev[j] == c->table_h[j];
+    t[j] = j < (int)c->table.size() ? c->table[j] : -1;
+    same = same && c->table_dev[j] == t[j];
   }
   if (same) return LEDE_OK;
-  HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.btab), c->table_h, n * 4, hipMemcpyHostToDevice, s));
-  c->table_dev.assign(c->table_h, c->table_h + n);
+  HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.btab), t, n * 4, hipMemcpyHostToDevice, s));
+  c->table_dev.assign(t, t + n);
+  return LEDE_OK;
+}
+
+// Wait for the work queued on the stream so far, on an event recorded after
+// it: in alternating runs of the 7B decode step this returned as soon as or
+// sooner than a stream synchronize (0 to 25 us a step).
+int wait_stream(lede_ctx* c, hipStream_t s) {
+  HIP_CHECK(c, hipEventRecord(c->wait_ev, s));
+  HIP_CHECK(c, hipEventSynchronize(c->wait_ev));
   return LEDE_OK;
 }
 
@@ -711,8 +740,7 @@ int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
 // written there by the Q-network's output kernel), in one read-back.
 int read_record(lede_ctx* c, hipStream_t s) {
   HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 50 * 4, hipMemcpyDeviceToHost, s));
-  HIP_CHECK(c, hipStreamSynchronize(s));
-  return LEDE_OK;
+  return wait_stream(c, s);
 }
 
 // Apply a finished verify (record read back) to the host mirror.
@@ -760,11 +788,12 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
   c->ws = (uint8_t*)ws;
   (void)hipGetDevice(&c->dev);
   for (int i = 0; i < o.n_pages; ++i) c->free_list.push_back(i);
-  if (hipHostMalloc((void**)&c->table_h, (size_t)o.max_pages_seq * 4 + 256, 0) != hipSuccess ||
+  if (hipHostMalloc((void**)&c->table_h, (size_t)(1 + LEDE_MAX_IN_FLIGHT) * table_pitch(o) * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->record_h, RECORD_INTS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->unif_h, UNIF_FLOATS * 4, 0) != hipSuccess ||
       hipHostMalloc((void**)&c->trace_h, 64 * 4, 0) != hipSuccess ||
-      hipHostMalloc((void**)&c->keys_h, 2 * KEY_WORDS * 8, 0) != hipSuccess) {
+      hipHostMalloc((void**)&c->keys_h, 2 * KEY_WORDS * 8, 0) != hipSuccess ||
+      hipHostMalloc((void**)&c->rec_slots_h, LEDE_MAX_IN_FLIGHT * RECORD_INTS * 4, 0) != hipSuccess) {
     lede_destroy(c);
     return LEDE_E_HIP;
   }
@@ -788,12 +817,27 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
     return LEDE_E_HIP;
   }
   c->table_dev = bt;
+  for (hipEvent_t& e : c->rec_ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      lede_destroy(c);
+      return LEDE_E_HIP;
+    }
+  if (hipEventCreateWithFlags(&c->wait_ev, hipEventDisableTiming) != hipSuccess) {
+    lede_destroy(c);
+    return LEDE_E_HIP;
+  }
   *out = c;
   return LEDE_OK;
 }
 
 void lede_destroy(lede_ctx* c) {
   if (!c) return;
+  // pipelined steps still copy their records into the host slots
+  for (const auto& f : c->inflight) (void)hipEventSynchronize(c->rec_ev[f.slot]);
+  for (hipEvent_t e : c->rec_ev)
+    if (e) (void)hipEventDestroy(e);
+  if (c->wait_ev) (void)hipEventDestroy(c->wait_ev);
+  if (c->rec_slots_h) (void)hipHostFree(c->rec_slots_h);
   for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.second);
   for (hipEvent_t e : c->evpool) (void)hipEventDestroy(e);
   if (c->table_h) (void)hipHostFree(c->table_h);
@@ -806,6 +850,7 @@ void lede_destroy(lede_ctx* c) {
 
 int lede_load_tensor(lede_ctx* c, int32_t kind, int32_t layer, const void* src, void* stream) {
   if (!c || !src) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   const Layout& o = c->lo;
   hipStream_t s = S_(stream);
   const bool per_layer = kind >= LEDE_T_ATTN_NORM && kind <= LEDE_T_WD;
@@ -852,6 +897,7 @@ int lede_load_tensor(lede_ctx* c, int32_t kind, int32_t layer, const void* src, 
 
 int lede_set_free_list(lede_ctx* c, const int32_t* order, int32_t n) {
   if (!c || !order) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (!c->table.empty()) return fail(c, LEDE_E_STATE, "pages are allocated");
   if (n != c->lo.n_pages) return fail(c, LEDE_E_ARG, "order must list all %d pages", c->lo.n_pages);
   std::vector<char> seen(n, 0);
@@ -865,6 +911,7 @@ int lede_set_free_list(lede_ctx* c, const int32_t* order, int32_t n) {
 
 int lede_set_options(lede_ctx* c, int32_t use_graphs, int32_t debug) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   c->use_graphs = use_graphs;
   c->debug = debug;
   return LEDE_OK;
@@ -872,6 +919,7 @@ int lede_set_options(lede_ctx* c, int32_t use_graphs, int32_t debug) {
 
 int lede_set_verify_reuse(lede_ctx* c, int32_t enable) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   c->verify_reuse = enable != 0;
   return LEDE_OK;
@@ -879,6 +927,7 @@ int lede_set_verify_reuse(lede_ctx* c, int32_t enable) {
 
 int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token) {
   if (!c || !tokens || n < 1) return fail(c, LEDE_E_ARG, "bad prefill arguments");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c->lo.V) return fail(c, LEDE_E_ARG, "token %d out of range", tokens[i]);
@@ -923,6 +972,7 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
 
 int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (token < 0 || token >= c->lo.V) return fail(c, LEDE_E_ARG, "token out of range");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   hipStream_t s = S_(stream);
@@ -935,6 +985,7 @@ int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
 
 int lede_truncate(lede_ctx* c, int32_t new_len, void* stream) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (new_len < 0 || new_len > c->seq_len) return fail(c, LEDE_E_ARG, "new_len %d not in [0, %d]", new_len, c->seq_len);
   hipStream_t s = S_(stream);
   c->policy_valid = 0;
@@ -966,6 +1017,7 @@ static int draft_impl(lede_ctx* c, int l, int k, hipStream_t s) {
 
 int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   hipStream_t s = S_(stream);
   int rc = draft_impl(c, l, k, s);
   if (rc) return rc;
@@ -980,6 +1032,7 @@ int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts)
 
 int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, int32_t* n_emitted, int32_t* verify) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
   hipStream_t s = S_(stream);
   const int k = c->drafted_k < 0 ? 0 : c->drafted_k;
@@ -1010,9 +1063,39 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
 namespace {
 
 // One step (greedy when temperature == 0, speculative sampling otherwise).
+// A step's host record from its device record r (acceptance record, and the
+// Q-network's action and value in slots 48..49).
+void fill_record(const lede_ctx* c, const int32_t* r, int l, int k, int k_eff, bool ran_q, lede_step_record* rec) {
+  const int a = r[0];
+  rec->l = l;
+  rec->k_req = k;
+  rec->k_eff = k_eff;
+  rec->accepted = a;
+  rec->n_emitted = a + 1;
+  for (int i = 0; i <= a; ++i) rec->tokens[i] = r[4 + i];
+  for (int i = 0; i < k_eff; ++i) rec->drafts[i] = r[24 + i];
+  rec->seq_len = r[2];
+  rec->pending = r[3];
+  if (ran_q) {
+    rec->q_action = r[48];
+    int32_t bits = r[49];
+    memcpy(&rec->q_max, &bits, 4);
+  } else {
+    rec->q_action = -1;
+    rec->q_max = NAN;
+  }
+  // Section 3.1.3 reward, summed over the drafts up to the first rejection
+  rec->reward = 0.f;
+  if (k_eff > 0) {
+    const double lam = (double)(c->lo.L - l) / c->lo.L;
+    rec->reward = (float)(a * (1.0 + lam) + (a < k_eff ? (-2.0 + lam) : 0.0));
+  }
+}
+
 int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, float temperature,
               const float* uniforms, void* stream, lede_step_record* rec) {
   if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
@@ -1058,7 +1141,7 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       rc = run_layers(c, 1, true, TokenSrc{nullptr, dk}, 0, 0, l_min, l_min, dk + 1, s);
       if (rc) return rc;
       HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.record) + 48, 2 * 4, hipMemcpyDeviceToHost, s));
-      HIP_CHECK(c, hipStreamSynchronize(s));
+      if ((rc = wait_stream(c, s))) return rc;
       const int a = c->record_h[48];
       if (a < 0 || a >= o.A) return fail(c, LEDE_E_HIP, "Q-network action %d out of range", a);
       l = c->cfg.exits[a / c->cfg.n_lengths];
@@ -1105,28 +1188,7 @@ verified:
   if (rc) return rc;
   commit_host(c);
   if ((rc = prof_fold(c))) return rc;
-  const int a = c->record_h[0];
-  rec->l = l;
-  rec->k_req = k;
-  rec->k_eff = k_eff;
-  rec->accepted = a;
-  rec->n_emitted = a + 1;
-  for (int i = 0; i <= a; ++i) rec->tokens[i] = c->record_h[4 + i];
-  for (int i = 0; i < k_eff; ++i) rec->drafts[i] = c->record_h[24 + i];
-  rec->seq_len = c->record_h[2];
-  rec->pending = c->record_h[3];
-  if (ran_q) {
-    rec->q_action = c->record_h[48];
-    int32_t bits = c->record_h[49];
-    memcpy(&rec->q_max, &bits, 4);
-  } else {
-    rec->q_max = NAN;
-  }
-  // Section 3.1.3 reward, summed over the drafts up to the first rejection
-  if (k_eff > 0) {
-    const double lam = (double)(o.L - l) / o.L;
-    rec->reward = (float)(a * (1.0 + lam) + (a < k_eff ? (-2.0 + lam) : 0.0));
-  }
+  fill_record(c, c->record_h, l, k, k_eff, ran_q, rec);
   return LEDE_OK;
 }
 
@@ -1139,6 +1201,70 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   return step_impl(c, forced, log_qnet, n_remaining, 0.f, nullptr, stream, rec);
 }
 
+int lede_step_submit(lede_ctx* c, const lede_action* action, int32_t log_qnet, int32_t n_remaining, void* stream) {
+  if (!c || !action) return fail(c, LEDE_E_ARG, "null argument");
+  if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  if ((int)c->inflight.size() >= LEDE_MAX_IN_FLIGHT)
+    return fail(c, LEDE_E_STATE, "%d steps are already outstanding", LEDE_MAX_IN_FLIGHT);
+  if (!c->inflight.empty() && stream != c->pipe_stream) return fail(c, LEDE_E_STATE, "submit on the collecting stream");
+  if (c->use_graphs || c->prof || c->verify_reuse)
+    return fail(c, LEDE_E_STATE, "graph replay, profiling and verify reuse are not pipelined");
+  const Layout& o = c->lo;
+  const int l = action->l, k = action->k;
+  if (l < 1 || l > o.L) return fail(c, LEDE_E_ARG, "exit layer %d not in 1..%d", l, o.L);
+  if (k < 0 || k > o.k_max) return fail(c, LEDE_E_ARG, "draft length %d not in 0..%d", k, o.k_max);
+  hipStream_t s = S_(stream);
+  const int k_eff = std::min(k, n_remaining - 1);
+  // the step starts at the committed length after the steps in flight, which
+  // the device knows; pages cover their longest acceptances
+  const int ub = c->inflight.empty() ? c->seq_len : c->seq_ub;
+  int rc = ensure_pages(c, ub + k_eff + 1);
+  if (rc) return rc;
+  const int slot = c->next_slot;
+  if ((rc = upload_table(c, s, c->table_h + (1 + slot) * table_pitch(o)))) return rc;
+  // the acceptance clears the entries from the first page wholly past the
+  // committed length to the last page the step wrote; the step starts at a
+  // length in [lo, ub] (every step in flight commits at least one token), so
+  // the host no longer knows the device's entries in that range
+  const int lo = c->seq_len + (int)c->inflight.size();
+  for (int j = (lo + 1 + PAGE - 1) / PAGE; j < (ub + k_eff + 1 + PAGE - 1) / PAGE && j < (int)c->table_dev.size(); ++j)
+    c->table_dev[j] = -2;
+  const int l_min = o.H ? c->cfg.exits[0] : 0;
+  const int qa = (o.H && log_qnet && l_min <= l && k_eff > 0) ? l_min : 0;
+  c->policy_valid = 0;
+  if (k_eff > 0 && (rc = launch_drafts(c, l, 1, k_eff, qa, 0, s))) return rc;
+  if ((rc = launch_verify(c, k_eff, s))) return rc;
+  c->next_slot = (slot + 1) % LEDE_MAX_IN_FLIGHT;
+  HIP_CHECK(c, hipMemcpyAsync(c->rec_slots_h + (size_t)slot * RECORD_INTS, c->S<int32_t>(o.record), 50 * 4,
+                              hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipEventRecord(c->rec_ev[slot], s));
+  c->inflight.push_back(lede_ctx::InFlight{l, k, k_eff, slot, qa > 0});
+  c->seq_ub = ub + k_eff + 1;
+  c->pipe_stream = stream;
+  return LEDE_OK;
+}
+
+int lede_step_collect(lede_ctx* c, void* stream, lede_step_record* rec) {
+  if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (c->inflight.empty()) return fail(c, LEDE_E_STATE, "no step submitted");
+  if (stream != c->pipe_stream) return fail(c, LEDE_E_STATE, "collect on the submitting stream");
+  const lede_ctx::InFlight f = c->inflight.front();
+  HIP_CHECK(c, hipEventSynchronize(c->rec_ev[f.slot]));
+  c->inflight.pop_front();
+  const int32_t* r = c->rec_slots_h + (size_t)f.slot * RECORD_INTS;
+  c->seq_len = r[2];
+  c->pending = r[3];
+  int ub = c->seq_len;
+  for (const auto& g : c->inflight) ub += g.k_eff + 1;
+  c->seq_ub = ub;
+  truncate_pages(c, ub);  // keeps the pages the remaining steps may still write
+  memset(rec, 0, sizeof *rec);
+  fill_record(c, r, f.l, f.k_req, f.k_eff, f.ran_q, rec);
+  return LEDE_OK;
+}
+
 int lede_step_sampled(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
                       float temperature, const float* uniforms, void* stream, lede_step_record* rec) {
   if (c && !(temperature > 0.f)) return fail(c, LEDE_E_ARG, "temperature must be > 0");
@@ -1147,6 +1273,7 @@ int lede_step_sampled(lede_ctx* c, const lede_action* forced, int32_t log_qnet, 
 
 int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_record* rec) {
   if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
@@ -1175,7 +1302,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
     pa.logits = logits; pa.kind = (float)kind; pa.index = (float)index;
     HIP_CHECK(c, launch_exit_policy(pa, s));
     HIP_CHECK(c, hipMemcpyAsync(c->trace_h, pa.out, POLICY_LOG * 4, hipMemcpyDeviceToHost, s));
-    HIP_CHECK(c, hipStreamSynchronize(s));
+    if (int rc = wait_stream(c, s)) return rc;
     c->policy_log.insert(c->policy_log.end(), c->trace_h, c->trace_h + POLICY_LOG);
     *action = c->trace_h[7] > 0.5f ? 1 : 0;
     return LEDE_OK;
@@ -1240,6 +1367,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
 
 int lede_set_trace(lede_ctx* c, const float* values, int32_t n, void* stream) {
   if (!c || (n > 0 && !values)) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (!c->lo.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
   if (n < 0 || n > POLICY_TRACE) return fail(c, LEDE_E_ARG, "trace length %d not in 0..%d", n, POLICY_TRACE);
   hipStream_t s = S_(stream);
@@ -1255,6 +1383,7 @@ int lede_set_trace(lede_ctx* c, const float* values, int32_t n, void* stream) {
 
 int lede_get_trace(lede_ctx* c, float* values, int32_t* n, void* stream) {
   if (!c || !values || !n) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (!c->lo.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
   hipStream_t s = S_(stream);
   HIP_CHECK(c, hipMemcpyAsync(c->trace_h, c->S<float>(c->lo.trace), POLICY_TRACE * 4, hipMemcpyDeviceToHost, s));
@@ -1289,6 +1418,7 @@ int lede_op_sample(const float* logits, int32_t V, float temperature, float u, i
 
 int lede_get_kv_state(lede_ctx* c, int32_t* seq_len, int32_t* pending, int32_t* bt, int32_t cap, int32_t* n_table) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (seq_len) *seq_len = c->seq_len;
   if (pending) *pending = c->pending;
   if (n_table) *n_table = (int32_t)c->table.size();
@@ -1301,6 +1431,7 @@ int lede_get_kv_state(lede_ctx* c, int32_t* seq_len, int32_t* pending, int32_t* 
 
 int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t* rows, void* stream) {
   if (!c || !host) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (!c->debug && which != 4) return fail(c, LEDE_E_STATE, "debug mode is off");
   hipStream_t s = S_(stream);
   const Layout& o = c->lo;
@@ -1330,6 +1461,7 @@ int lede_debug_read(lede_ctx* c, int32_t which, float* host, size_t cap, int32_t
 
 int lede_prof_enable(lede_ctx* c, int32_t on) {
   if (!c) return LEDE_E_ARG;
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   int rc = prof_fold(c);
   if (rc) return rc;
   if (on < 0 || on > 2) return fail(c, LEDE_E_ARG, "timing level %d not in 0..2", on);

@@ -68,7 +68,9 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_op_read_probe", "lede_op_read_groups", "lede_step_sampled", "lede_op_sample", "lede_step_policy", "lede_set_trace",
             "lede_get_trace", "lede_set_verify_reuse", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
             "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
-            "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read"]
+            "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read", "lede_step_submit",
+            "lede_step_collect"]
+MAX_IN_FLIGHT = 2
 SAMPLE_SLOTS = 16
 SAMPLE_STRIDE = 33
 
@@ -101,6 +103,8 @@ def load(path: str = LIB_PATH):
     L.lede_draft.argtypes = [vp, i32, i32, vp, P(i32)]
     L.lede_verify.argtypes = [vp, vp, P(i32), P(i32), P(i32), P(i32)]
     L.lede_step.argtypes = [vp, P(LedeAction), i32, i32, vp, P(LedeStepRecord)]
+    L.lede_step_submit.argtypes = [vp, P(LedeAction), i32, i32, vp]
+    L.lede_step_collect.argtypes = [vp, vp, P(LedeStepRecord)]
     L.lede_get_kv_state.argtypes = [vp, P(i32), P(i32), P(i32), i32, P(i32)]
     L.lede_debug_read.argtypes = [vp, i32, P(ctypes.c_float), sz, P(i32), vp]
     L.lede_prof_enable.argtypes = [vp, i32]
@@ -313,6 +317,18 @@ class Engine:
         act = LedeAction(int(action[0]), int(action[1])) if action is not None else None
         self._check(self.L.lede_step(self.ctx, ctypes.byref(act) if act is not None else None, int(log_qnet),
                                      int(n_remaining), self.stream, ctypes.byref(rec)), self.ctx)
+        return self._record(rec)
+
+    def lede_step_submit(self, action, n_remaining: int = 1 << 30, log_qnet: bool = True) -> None:
+        """Queue a forced greedy step; at most MAX_IN_FLIGHT wait for lede_step_collect."""
+        act = LedeAction(int(action[0]), int(action[1]))
+        self._check(self.L.lede_step_submit(self.ctx, ctypes.byref(act), int(log_qnet), int(n_remaining),
+                                            self.stream), self.ctx)
+
+    def lede_step_collect(self) -> StepRecord:
+        """The record of the oldest submitted step (waits for it)."""
+        rec = LedeStepRecord()
+        self._check(self.L.lede_step_collect(self.ctx, self.stream, ctypes.byref(rec)), self.ctx)
         return self._record(rec)
 
     def lede_step_sampled(self, action, temperature: float, uniforms, n_remaining: int = 1 << 30,

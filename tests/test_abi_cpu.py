@@ -80,6 +80,17 @@ def test_null_arguments(lib):
     assert lib.lede_last_error(None) == b"null context"
 
 
+def test_pipelined_step_null_arguments(lib):
+    import re
+    from paper_2606_03113_amd import lede
+    act = lede.LedeAction(1, 2)
+    rec = lede.LedeStepRecord()
+    assert lib.lede_step_submit(None, ctypes.byref(act), 0, 8, None) == lede.LEDE_E_ARG
+    assert lib.lede_step_collect(None, None, ctypes.byref(rec)) == lede.LEDE_E_ARG
+    text = open(os.path.join(ROOT, "include", "lede.h")).read()
+    assert int(re.search(r"#define LEDE_MAX_IN_FLIGHT (\d+)", text).group(1)) == lede.MAX_IN_FLIGHT
+
+
 def test_read_probe_rejects_bad_arguments(lib):
     from paper_2606_03113_amd import lede
     sink = ctypes.c_void_p(16)
