@@ -48,26 +48,24 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   // values (dims dg*8.., tokens tg + PV_TG u)
   const int dg = tid % PV_DG, tg = tid / PV_DG;
   float vf[TPT][8], kf[NPC * 8];
+  // Every token slot of an allocated page is readable, so the loads are
+  // unconditional and tokens past the length are zeroed afterwards: guarded
+  // loads compile to one branch and one wait per load.
   auto load_page = [&](int jj) {
     const int page = a.block_table[jj];
     const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
     const int nvalid = min(64, pmax - jj * 64 + 1);
 #pragma unroll
-    for (int u = 0; u < TPT; ++u) {
-      const int t = tg + PV_TG * u;
-      if (t < nvalid) load8<DT>(a.vcache, base + (size_t)t * HD + dg * 8, vf[u]);
-      else
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vf[u][e] = 0.f;
-    }
+    for (int u = 0; u < TPT; ++u) load8<DT>(a.vcache, base + (size_t)(tg + PV_TG * u) * HD + dg * 8, vf[u]);
     const int t = tid >> 2, p = tid & 3;
-    if (t < nvalid) {
 #pragma unroll
-      for (int c = 0; c < NPC; ++c) load8<DT>(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c, kf + 8 * c);
-    } else {
+    for (int c = 0; c < NPC; ++c) load8<DT>(a.kcache, base + (size_t)t * HD + p * 8 + 32 * c, kf + 8 * c);
 #pragma unroll
-      for (int e = 0; e < NPC * 8; ++e) kf[e] = 0.f;
-    }
+    for (int u = 0; u < TPT; ++u)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vf[u][e] = tg + PV_TG * u < nvalid ? vf[u][e] : 0.f;
+#pragma unroll
+    for (int e = 0; e < NPC * 8; ++e) kf[e] = t < nvalid ? kf[e] : 0.f;
   };
   load_page(blockIdx.y);  // the first page's keys and values are in flight with the query loads
 
@@ -147,26 +145,33 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
-// Combine the per-page partials of every (row, head) in page order (up to
-// 16 pages requested at once: one round trip for a 1024-token context).
+// Combine the per-page partials of every (row, head) in page order, 16
+// pages per round trip: the loads are unconditional (a page index past the
+// buffer is clamped to its last page, and pages past the row's position are
+// loaded but not folded), so they issue together instead of one guarded
+// load after another, and the first 16 go out with the sequence length.
 template <int DT, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
   constexpr int B = 16;
   const int m = blockIdx.x / a.nq, head = blockIdx.x % a.nq, i = threadIdx.x;
-  const int pos = *a.seq_len + a.pos_off + m;
-  const int nc = pos / 64 + 1;
   const float* p = a.part + ((size_t)m * a.nq + head) * a.max_chunks * (HD + 2);
-  float mx = -INFINITY, l = 0.f, acc = 0.f;
-  for (int j0 = 0; j0 < nc; j0 += B) {
-    float pm[B], pl[B], pa[B];
+  float pm[B], pl[B], pa[B];
+  auto load = [&](int j0) {
 #pragma unroll
     for (int u = 0; u < B; ++u) {
-      const float* q = p + (size_t)(j0 + u) * (HD + 2);
-      const bool ok = j0 + u < nc;
-      pm[u] = ok ? q[0] : -INFINITY;
-      pl[u] = ok ? q[1] : 0.f;
-      pa[u] = ok ? q[2 + i] : 0.f;
+      const float* q = p + (size_t)min(j0 + u, a.max_chunks - 1) * (HD + 2);
+      pm[u] = q[0];
+      pl[u] = q[1];
+      pa[u] = q[2 + i];
     }
+  };
+  load(0);
+  const int pos = *a.seq_len + a.pos_off + m;
+  const int nc = pos / 64 + 1;
+  __builtin_assume(nc >= 1);  // lets the first loads issue before the length arrives
+  float mx = -INFINITY, l = 0.f, acc = 0.f;
+  for (int j0 = 0; j0 < nc; j0 += B) {
+    if (j0 > 0) load(j0);
 #pragma unroll
     for (int u = 0; u < B; ++u) {
       if (j0 + u >= nc) break;
@@ -233,17 +238,21 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
   {
     const float scale = rsqrtf((float)HD);
     const float* qp = a.q + (size_t)m_row * a.ldq + head * HD + lg * 8;
+    // unconditional loads (a row past nr reads row 0's query, then zeroes it)
+    float4 qu[KS], qv[KS];
 #pragma unroll
     for (int s2 = 0; s2 < KS; ++s2) {
-      float x[8];
-      if (row_ok) {
-        const float4 u = *(const float4*)(qp + 32 * s2), v = *(const float4*)(qp + 32 * s2 + 4);
-        x[0] = u.x * scale; x[1] = u.y * scale; x[2] = u.z * scale; x[3] = u.w * scale;
-        x[4] = v.x * scale; x[5] = v.y * scale; x[6] = v.z * scale; x[7] = v.w * scale;
-      } else {
+      qu[s2] = *(const float4*)(qp + 32 * s2);
+      qv[s2] = *(const float4*)(qp + 32 * s2 + 4);
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) x[e] = 0.f;
-      }
+    for (int s2 = 0; s2 < KS; ++s2) {
+      const float4 u = qu[s2], v = qv[s2];
+      float x[8];
+      x[0] = row_ok ? u.x * scale : 0.f; x[1] = row_ok ? u.y * scale : 0.f;
+      x[2] = row_ok ? u.z * scale : 0.f; x[3] = row_ok ? u.w * scale : 0.f;
+      x[4] = row_ok ? v.x * scale : 0.f; x[5] = row_ok ? v.y * scale : 0.f;
+      x[6] = row_ok ? v.z * scale : 0.f; x[7] = row_ok ? v.w * scale : 0.f;
       split8(x, qh[s2], ql[s2]);
     }
   }
@@ -254,17 +263,29 @@ __global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
     const size_t base = (((size_t)a.layer * a.n_pages + page) * a.nkv + kvh) * 64 * HD;
     const int nvalid = min(64, pmax - j * 64 + 1);
     // keys of tokens 16w + lr, dims 32 s + 8 lg; values of this wavefront's dims
+    // (unconditional loads within the page, tokens past the length zeroed after)
     uint4 kf[KS];
     const int tk = 16 * w + lr;
 #pragma unroll
-    for (int s2 = 0; s2 < KS; ++s2)
-      kf[s2] = tk < nvalid ? ld16(kc + base + (size_t)tk * HD + 32 * s2 + 8 * lg) : make_uint4(0u, 0u, 0u, 0u);
+    for (int s2 = 0; s2 < KS; ++s2) kf[s2] = ld16(kc + base + (size_t)tk * HD + 32 * s2 + 8 * lg);
     constexpr int VC = 64 * DW / 8 / 64;   // 16-byte value chunks per lane
     uint4 vf[VC];
 #pragma unroll
     for (int c = 0; c < VC; ++c) {
       const int idx = l + 64 * c, t = idx / (DW / 8), d8 = idx % (DW / 8);
-      vf[c] = t < nvalid ? ld16(vc + base + (size_t)t * HD + w * DW + 8 * d8) : make_uint4(0u, 0u, 0u, 0u);
+      vf[c] = ld16(vc + base + (size_t)t * HD + w * DW + 8 * d8);
+    }
+    // (masks, not selects of whole vectors: those select addresses and
+    // put the arrays in scratch)
+    const uint32_t km = tk < nvalid ? ~0u : 0u;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      kf[s2].x &= km; kf[s2].y &= km; kf[s2].z &= km; kf[s2].w &= km;
+    }
+#pragma unroll
+    for (int c = 0; c < VC; ++c) {
+      const uint32_t vm = (l + 64 * c) / (DW / 8) < nvalid ? ~0u : 0u;
+      vf[c].x &= vm; vf[c].y &= vm; vf[c].z &= vm; vf[c].w &= vm;
     }
     // S^T tile: lane holds tokens 16w + 4 lg + i of row lr
     f32x4 sc = {0.f, 0.f, 0.f, 0.f};
