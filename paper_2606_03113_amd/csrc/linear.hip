@@ -234,12 +234,35 @@ __device__ __forceinline__ void norm_row_load(const LinearArgs& a, NormRow<NW>& 
     row = (const uint8_t*)a.embed + (size_t)tok * a.K * Elem<DT>::ES_;
     h = nullptr;
   }
+  // unconditional loads (a lane past the row re-reads its first elements),
+  // zeroed afterwards: guarded loads compile to a branch and a wait each
+  // (the gain first, then the row from a source chosen once, outside the
+  // loops, so that no branch separates the loads)
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int i = 4 * tid + 4 * NT * j;
-    const bool in = i < a.K;
-    nr.v[j] = in ? row_load4<DT>(h, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    nr.g[j] = in ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    nr.g[j] = row_load4<DT>(nullptr, a.gain, i < a.K ? i : 0);
+  }
+  if (h) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int i = 4 * tid + 4 * NT * j;
+      nr.v[j] = row_load4<DT>(h, nullptr, i < a.K ? i : 0);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int i = 4 * tid + 4 * NT * j;
+      nr.v[j] = row_load4<DT>(nullptr, row, i < a.K ? i : 0);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const bool in = 4 * tid + 4 * NT * j < a.K;
+    nr.v[j].x = in ? nr.v[j].x : 0.f; nr.v[j].y = in ? nr.v[j].y : 0.f;
+    nr.v[j].z = in ? nr.v[j].z : 0.f; nr.v[j].w = in ? nr.v[j].w : 0.f;
+    nr.g[j].x = in ? nr.g[j].x : 0.f; nr.g[j].y = in ? nr.g[j].y : 0.f;
+    nr.g[j].z = in ? nr.g[j].z : 0.f; nr.g[j].w = in ? nr.g[j].w : 0.f;
   }
 }
 

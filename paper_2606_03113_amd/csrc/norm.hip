@@ -21,12 +21,33 @@ __global__ __launch_bounds__(256) void k_norm(NormArgs a) {
     row = (const uint8_t*)a.embed_w + (size_t)tok * a.d * Elem<DT>::ES_;
     src = nullptr;
   }
+  // unconditional loads (a thread past the row re-reads its first elements),
+  // zeroed afterwards, and the row's source chosen outside the loops: a
+  // guarded load compiles to a branch and a wait
   float4 v[8], g[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int i = 4 * tid + 1024 * j;
-    v[j] = i < a.d ? row_load4<DT>(src, row, i) : make_float4(0.f, 0.f, 0.f, 0.f);
-    g[j] = i < a.d ? row_load4<DT>(nullptr, a.gain, i) : make_float4(0.f, 0.f, 0.f, 0.f);
+    g[j] = row_load4<DT>(nullptr, a.gain, i < a.d ? i : 0);
+  }
+  if (src) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = 4 * tid + 1024 * j;
+      v[j] = row_load4<DT>(src, nullptr, i < a.d ? i : 0);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int i = 4 * tid + 1024 * j;
+      v[j] = row_load4<DT>(nullptr, row, i < a.d ? i : 0);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const bool in = 4 * tid + 1024 * j < a.d;
+    v[j].x = in ? v[j].x : 0.f; v[j].y = in ? v[j].y : 0.f; v[j].z = in ? v[j].z : 0.f; v[j].w = in ? v[j].w : 0.f;
+    g[j].x = in ? g[j].x : 0.f; g[j].y = in ? g[j].y : 0.f; g[j].z = in ? g[j].z : 0.f; g[j].w = in ? g[j].w : 0.f;
   }
   float ss = 0.f;
 #pragma unroll
