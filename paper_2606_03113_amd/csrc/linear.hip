@@ -100,10 +100,13 @@ __device__ __forceinline__ void epilogue(const LinearArgs& a, int g, float (*ct)
       if (m < M) {
         const int col = g * 16 + n;
         float* hp = a.h + (size_t)m * a.ldh + col;
+        // the gain is read before the residual is stored, so that the two
+        // loads share one round trip (after the store they could alias)
+        const float gn = a.ss_out ? Elem<DT>::load(a.xg_gain, col) : 0.f;
         const float hn = *hp + ct[n][m];
         *hp = hn;
         if (a.ss_out) {
-          Elem<DT>::store(a.xg, (size_t)m * a.ldxg + col, hn * Elem<DT>::load(a.xg_gain, col));
+          Elem<DT>::store(a.xg, (size_t)m * a.ldxg + col, hn * gn);
           ct[n][m] = hn;  // squared and summed per row once the block has synchronised
         }
       }
