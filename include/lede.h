@@ -205,8 +205,9 @@ int lede_verify(lede_ctx* ctx, void* stream, int32_t* accepted, int32_t* tokens,
 int lede_step(lede_ctx* ctx, const lede_action* forced, int32_t log_qnet, int32_t n_remaining,
               void* stream, lede_step_record* rec);
 
-/* Pipelined steps (the same step as lede_step with a forced action, greedy
- * acceptance): lede_step_submit enqueues the whole step on `stream` (drafts,
+/* Pipelined steps (the same step as lede_step with a forced action: drafts
+ * and verify of Section 2.2, greedy acceptance and rollback of Section 3.3,
+ * the Section 3.1.3 reward in the record): lede_step_submit enqueues the whole step on `stream` (drafts,
  * verify, acceptance, and the record's read-back into a host slot) and
  * returns without waiting; lede_step_collect waits for the oldest submitted
  * step and fills *rec exactly as lede_step would have.  The device holds the
