@@ -175,6 +175,12 @@ struct lede_ctx {
   int32_t* rec_slots_h = nullptr;          // pinned [LEDE_MAX_IN_FLIGHT][RECORD_INTS]
   hipEvent_t rec_ev[LEDE_MAX_IN_FLIGHT] = {};
   hipEvent_t wait_ev = nullptr;            // the read-backs of a synchronous step wait on it
+  // A forced step's logged Q-network runs on a second stream (default
+  // priority) after its input row is normalised, beside the rest of the
+  // draft pass; the record's read-back waits for it.
+  hipStream_t side = nullptr;
+  hipEvent_t side_in = nullptr, side_out = nullptr;
+  int qnet_defer = 0, side_pending = 0;
   int next_slot = 0;
   int seq_ub = 0;                          // committed length after every step in flight, at most
   void* pipe_stream = nullptr;
@@ -369,6 +375,16 @@ int upload_table(lede_ctx* c, hipStream_t s, int32_t* stage = nullptr) {
   return LEDE_OK;
 }
 
+// Order the stream after a deferred Q-network (its action and maximum are in
+// the record).
+int join_side(lede_ctx* c, hipStream_t s) {
+  if (c->side_pending) {
+    HIP_CHECK(c, hipStreamWaitEvent(s, c->side_out, 0));
+    c->side_pending = 0;
+  }
+  return LEDE_OK;
+}
+
 // Wait for the work queued on the stream so far, on an event recorded after
 // it: in alternating runs of the 7B decode step this returned as soon as or
 // sooner than a stream synchronize (0 to 25 us a step).
@@ -559,17 +575,33 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       na.h = hrow; na.gain = c->W<void>(o.final_norm); na.eps = c->cfg.rms_eps;
       na.x = c->S<void>(o.qs); na.f32_out = 1;
       LAUNCH(LEDE_K_QNET, (double)o.d * 8, launch_norm(dt, na, s));
+      // the hidden and output layers read only the normalised row: on the
+      // second stream when the step's caller does not wait for the action
+      const bool defer = c->qnet_defer && c->side && !c->prof;
+      hipStream_t qstream = s;
+      if (defer) {
+        HIP_CHECK(c, hipEventRecord(c->side_in, s));
+        HIP_CHECK(c, hipStreamWaitEvent(c->side, c->side_in, 0));
+        qstream = c->side;
+      }
       LinearArgs la = base_linear(c);
       la.w = c->W<uint8_t>(o.qw1);
       la.n_groups = o.H / 16; la.KT = k_tiles(0, o.d); la.K = o.d;
       la.x_mode = X_F32; la.x = c->S<void>(o.qs);
       la.epi = EPI_BIAS_RELU; la.out = c->S<float>(o.qhid); la.bias = c->W<float>(o.qb1);
-      LAUNCH(LEDE_K_QNET, linear_bytes(la, 0), launch_linear(0, false, la, la.n_groups, s));
       QnetOutArgs qo{};
       qo.hid = c->S<float>(o.qhid); qo.H = o.H;
       qo.w2 = c->W<float>(o.qw2); qo.b2 = c->W<float>(o.qb2); qo.A = o.A;
       qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.record) + 48;
-      LAUNCH(LEDE_K_QNET, (double)o.A * (o.H + 2) * 4, launch_qnet_out(qo, s));
+      if (defer) {
+        HIP_CHECK(c, launch_linear(0, false, la, la.n_groups, qstream));
+        HIP_CHECK(c, launch_qnet_out(qo, qstream));
+        HIP_CHECK(c, hipEventRecord(c->side_out, qstream));
+        c->side_pending = 1;
+      } else {
+        LAUNCH(LEDE_K_QNET, linear_bytes(la, 0), launch_linear(0, false, la, la.n_groups, s));
+        LAUNCH(LEDE_K_QNET, (double)o.A * (o.H + 2) * 4, launch_qnet_out(qo, s));
+      }
     }
   }
   return LEDE_OK;
@@ -739,6 +771,7 @@ int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
 // The acceptance record, and the Q-network's action and value (slots 48..49,
 // written there by the Q-network's output kernel), in one read-back.
 int read_record(lede_ctx* c, hipStream_t s) {
+  if (int rc = join_side(c, s)) return rc;
   HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 50 * 4, hipMemcpyDeviceToHost, s));
   return wait_stream(c, s);
 }
@@ -822,7 +855,10 @@ int lede_create(const lede_config* cfg, void* warena, size_t wbytes, void* kv, s
       lede_destroy(c);
       return LEDE_E_HIP;
     }
-  if (hipEventCreateWithFlags(&c->wait_ev, hipEventDisableTiming) != hipSuccess) {
+  if (hipEventCreateWithFlags(&c->wait_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->side_in, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&c->side_out, hipEventDisableTiming) != hipSuccess ||
+      hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking) != hipSuccess) {
     lede_destroy(c);
     return LEDE_E_HIP;
   }
@@ -837,6 +873,12 @@ void lede_destroy(lede_ctx* c) {
   for (hipEvent_t e : c->rec_ev)
     if (e) (void)hipEventDestroy(e);
   if (c->wait_ev) (void)hipEventDestroy(c->wait_ev);
+  if (c->side) {
+    (void)hipStreamSynchronize(c->side);
+    (void)hipStreamDestroy(c->side);
+  }
+  if (c->side_in) (void)hipEventDestroy(c->side_in);
+  if (c->side_out) (void)hipEventDestroy(c->side_out);
   if (c->rec_slots_h) (void)hipHostFree(c->rec_slots_h);
   for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.second);
   for (hipEvent_t e : c->evpool) (void)hipEventDestroy(e);
@@ -1162,7 +1204,9 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
         if ((rc = step_graph(c, l, k_eff, qa, s))) { truncate_pages(c, c0); return rc; }
         goto verified;
       }
+      c->qnet_defer = 1;
       rc = launch_drafts(c, l, 1, k_eff, qa, 0, s, inv_t);
+      c->qnet_defer = 0;
       if (rc) return rc;
     }
   } else {
@@ -1234,8 +1278,12 @@ int lede_step_submit(lede_ctx* c, const lede_action* action, int32_t log_qnet, i
   const int l_min = o.H ? c->cfg.exits[0] : 0;
   const int qa = (o.H && log_qnet && l_min <= l && k_eff > 0) ? l_min : 0;
   c->policy_valid = 0;
-  if (k_eff > 0 && (rc = launch_drafts(c, l, 1, k_eff, qa, 0, s))) return rc;
+  c->qnet_defer = 1;
+  rc = k_eff > 0 ? launch_drafts(c, l, 1, k_eff, qa, 0, s) : LEDE_OK;
+  c->qnet_defer = 0;
+  if (rc) return rc;
   if ((rc = launch_verify(c, k_eff, s))) return rc;
+  if ((rc = join_side(c, s))) return rc;
   c->next_slot = (slot + 1) % LEDE_MAX_IN_FLIGHT;
   HIP_CHECK(c, hipMemcpyAsync(c->rec_slots_h + (size_t)slot * RECORD_INTS, c->S<int32_t>(o.record), 50 * 4,
                               hipMemcpyDeviceToHost, s));
