@@ -8,15 +8,16 @@ namespace lede {
 
 // Commit of a verified step: the record, the new length, the pending token
 // and the device block table (pages wholly past the committed length go back
-// to the pool).  One thread.
-__device__ void commit_step(const AcceptArgs& a, int acc, int y) {
+// to the pool).  One thread.  drafts: the decoded drafts (index 1..k) if
+// the caller has them, else they are decoded from the keys here.
+__device__ void commit_step(const AcceptArgs& a, int acc, int y, const int* drafts = nullptr) {
   TokenSrc dk = {nullptr, a.dkeys};
   const int k = a.k;
   const int c = *a.seq_len;
   const int c_new = c + acc + 1;
-  for (int i = 0; i < acc; ++i) a.record[4 + i] = dk.get(i + 1);
+  for (int i = 0; i < acc; ++i) a.record[4 + i] = drafts ? drafts[i + 1] : dk.get(i + 1);
   a.record[4 + acc] = y;
-  for (int i = 0; i < k; ++i) a.record[24 + i] = dk.get(i + 1);
+  for (int i = 0; i < k; ++i) a.record[24 + i] = drafts ? drafts[i + 1] : dk.get(i + 1);
   a.record[0] = acc;
   a.record[1] = acc + 1;
   a.record[2] = c_new;
@@ -27,13 +28,23 @@ __device__ void commit_step(const AcceptArgs& a, int acc, int y) {
   for (int j = keep; j < used; ++j) a.block_table[j] = -1;
 }
 
+// Lanes 0..k decode verify row i's argmax and draft i at once (each the
+// largest of a key's slot words); lane 0 then scans for the first mismatch
+// and commits.  k is at most 15 (the configuration's limit on k_max).
 __global__ void k_accept(AcceptArgs a) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  TokenSrc dk = {nullptr, a.dkeys}, vk = {nullptr, a.vkeys};
-  const int k = a.k;
+  constexpr int KM = 15;
+  __shared__ int dtok[KM + 1], vtok[KM + 1];
+  const int i = threadIdx.x, k = min(a.k, KM);
+  if (blockIdx.x != 0) return;
+  if (i <= k) {
+    vtok[i] = TokenSrc{nullptr, a.vkeys}.get(i);
+    dtok[i] = i ? TokenSrc{nullptr, a.dkeys}.get(i) : 0;
+  }
+  __syncthreads();
+  if (i != 0) return;
   int acc = 0;
-  while (acc < k && dk.get(acc + 1) == vk.get(acc)) ++acc;
-  commit_step(a, acc, vk.get(acc));
+  while (acc < k && dtok[acc + 1] == vtok[acc]) ++acc;
+  commit_step(a, acc, vtok[acc], dtok);
 }
 
 // ---- speculative sampling -------------------------------------------------------
