@@ -152,3 +152,33 @@ def test_pipeline_state_errors():
     eng.lede_set_options(0, 0)
     eng.lede_set_verify_reuse(True)
     assert code(eng.lede_step_submit, (1, 2)) == LEDE_E_STATE  # nor verify reuse
+
+
+def test_steps_on_a_created_stream():
+    """Forced steps with the Q-network logged (its hidden and output layers
+    run on the library's second stream) on a stream the caller created, plain
+    and pipelined, against the same steps on the default stream."""
+    model = TINY_BF16
+    w, q = li.weights(model), li.qnet_weights(model)
+    order = list(range(MAX_CTX // 64))
+    ref, eng = _engine(model, w, q, order), _engine(model, w, q, order)
+    prompt = li.uniform_int(3, 52, 40, 0, model.vocab - 1)
+    L = model.n_layers
+    sched = [(1, 4), (L, 8), (2, 0), (L, 2), (1, 12), (2, 3)] * 3
+    g = ref.lede_prefill(prompt)
+    want = [ref.lede_step(a, log_qnet=True) for a in sched]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        assert eng.lede_prefill(prompt) == g
+        half = len(sched) // 2
+        got = [eng.lede_step(a, log_qnet=True) for a in sched[:half]]
+        for i, a in enumerate(sched[half:]):
+            if i >= 2:
+                got.append(eng.lede_step_collect())
+            eng.lede_step_submit(a, log_qnet=True)
+        while len(got) < len(sched):
+            got.append(eng.lede_step_collect())
+    torch.cuda.synchronize()
+    assert any(r.q_action >= 0 for r in want)
+    for i, (a, b) in enumerate(zip(want, got)):
+        assert _fields(a) == _fields(b), (i, sched[i], a, b)
