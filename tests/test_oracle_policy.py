@@ -153,4 +153,5 @@ def test_trace_follows_committed_tokens():
         r = st.step_paper(30, _const_policy(1), k_cap=3)
         n += len(r.emitted)
         assert len(st.trace.vals) == min(n, POLICY_TRACE)
-        assert r.c_trace == pytest.approx(r.c_trace)
+    # the values themselves are pinned against the brute-force full model in
+    # tests/test_oracle_trace.py
