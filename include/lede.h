@@ -14,8 +14,15 @@
  *
  * Conventions for every entry point:
  *  - Return value: LEDE_OK (0) or a negative lede_status.  On error the
- *    decoding state (KV length, pending token, page table) is unchanged and
- *    lede_last_error() describes the failure.  No exception crosses the ABI.
+ *    decoding state (KV length, pending token, page table, the exit policy's
+ *    confidence trace) is the one the call started from -- a call that fails
+ *    after it has allocated pages or issued device work drains the stream
+ *    and rewrites the device's copies of that state -- and lede_last_error()
+ *    describes the failure.  A failed draft, verify or step also leaves no
+ *    draft outstanding: the transition of Section 3.1 (draft, verify,
+ *    commit) rolls back to the committed state.  KV entries past the
+ *    committed length may have been overwritten; they are never read.  No
+ *    exception crosses the ABI.
  *  - Device pointers are HIP device addresses on the current device; host
  *    pointers are ordinary process memory.  The caller owns every buffer it
  *    passes (weights staging, weight arena, KV pool, workspace) and the
@@ -91,6 +98,23 @@ typedef enum {
   LEDE_T_EXIT_W1, LEDE_T_EXIT_B1, LEDE_T_EXIT_W2, LEDE_T_EXIT_B2
 } lede_tensor;
 
+/* Every tensor of the model at once, for lede_load_weights: device pointers
+ * (non-owning; read on the stream of the call) in the logical layouts of
+ * lede_load_tensor.  A null pointer leaves that tensor as it is, so a
+ * caller short of device memory may load a model in several calls (for
+ * example a range of layers at a time).  `layer` is a host array of
+ * n_layers * LEDE_LAYER_TENSORS pointers for layers first_layer ..
+ * first_layer + n_layers - 1, in the order attn_norm, wq, wk, wv, wo,
+ * ffn_norm, wg, wu, wd. */
+#define LEDE_LAYER_TENSORS 9
+typedef struct {
+  const void *embed, *final_norm, *head;
+  int32_t first_layer, n_layers;
+  const void* const* layer;
+  const float *qnet_w1, *qnet_b1, *qnet_w2, *qnet_b2;  /* the (exit, length) Q-network */
+  const float *exit_w1, *exit_b1, *exit_w2, *exit_b2;  /* the exit policy's 2-action Q-network */
+} lede_weights;
+
 /* An action of the agent: exit layer l* (1..L) and draft length k. */
 typedef struct {
   int32_t l, k;
@@ -139,13 +163,26 @@ const char* lede_last_error(const lede_ctx* ctx);
  * this call. */
 int lede_load_tensor(lede_ctx* ctx, int32_t kind, int32_t layer, const void* src, void* stream);
 
+/* Load the weights of the decoder the MDP runs on (Section 3.1: the states
+ * are its hidden states, the actions its exit layers; Section 2.2: the draft
+ * model is its own first layers with the shared final norm and LM head) and
+ * of its Q-networks (Section 3.2), repacking every non-null tensor of *w as
+ * lede_load_tensor does, in the order embed, final_norm, head, layers, Q-network,
+ * exit policy.  LEDE_E_ARG on a null ctx or w, a layer range outside the
+ * model or a null layer table with n_layers > 0; LEDE_E_STATE when a
+ * Q-network tensor is given to a config without that network; LEDE_E_HIP on
+ * a failed repack (tensors before it are loaded).  Stream-ordered; the
+ * sources may be reused once the stream has passed the call. */
+int lede_load_weights(lede_ctx* ctx, const lede_weights* w, void* stream);
+
 /* Seed the KV page free list with a permutation of 0..n_pages-1 (allocation
  * pops the front).  Only valid while no page is allocated. */
 int lede_set_free_list(lede_ctx* ctx, const int32_t* order, int32_t n);
 
 /* Options: use_graphs -- replay each step shape as a captured HIP graph;
  * debug -- keep the fp32 logits of the last draft / verify / prefill head
- * and the Q-values for lede_debug_read. */
+ * and the Q-values for lede_debug_read.  Changing either drops the captured
+ * graphs (a capture holds the debug mode it was made in). */
 int lede_set_options(lede_ctx* ctx, int32_t use_graphs, int32_t debug);
 
 /* Verify reuse (the self-speculative decoding the paper builds on, Section
@@ -164,18 +201,28 @@ int lede_set_options(lede_ctx* ctx, int32_t use_graphs, int32_t debug);
  * outstanding. */
 int lede_set_verify_reuse(lede_ctx* ctx, int32_t enable);
 
-/* Append n prompt tokens (host int32, each in [0, vocab)) at positions
- * seq_len .. seq_len+n-1 through all L layers, writing their K/V; the
- * argmax of the last row becomes the pending token and is returned in
- * *next_token (host).  Valid when no draft is outstanding.  Synchronises. */
+/* Prefill (the paper does not describe it; decoding in Section 4.1 starts
+ * from a prompt at batch 1): append n prompt tokens (host int32, each in
+ * [0, vocab)) at positions seq_len .. seq_len+n-1 through all L layers in
+ * 16-row passes of the verify kernels, writing their K/V; the full model's
+ * argmax at the last row becomes the pending token and is returned in
+ * *next_token (host), and its -log max p enters the confidence trace.
+ * Valid when no draft is outstanding (LEDE_E_STATE); LEDE_E_ARG on a null
+ * pointer, n < 1 or a token out of range; LEDE_E_CTX_OVERFLOW /
+ * LEDE_E_KV_FULL when the positions do not fit.  Synchronises. */
 int lede_prefill(lede_ctx* ctx, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token);
 
 /* Replace the pending token (teacher forcing / resume).  Synchronous. */
 int lede_set_pending(lede_ctx* ctx, int32_t token, void* stream);
 
-/* Roll the sequence back to new_len <= seq_len positions: frees the pages
- * wholly past it (pushed to the front of the free list in descending
- * logical order) and discards any outstanding draft. */
+/* KV rollback (the paper leaves it implicit: a transition of Section 3.1
+ * commits only the accepted drafts and the verify token, so the positions
+ * of rejected drafts are dropped; this call exposes the same truncation for
+ * resume and teacher forcing): roll the sequence back to new_len <= seq_len
+ * positions, free the pages wholly past it (pushed to the front of the free
+ * list in descending logical order) and discard any outstanding draft.  The
+ * pending token is unchanged (lede_set_pending or lede_prefill sets the next
+ * one).  LEDE_E_ARG when new_len is outside [0, seq_len]. */
 int lede_truncate(lede_ctx* ctx, int32_t new_len, void* stream);
 
 /* Draft k >= 1 tokens from the pending token by running layers 1..l (Section
@@ -185,12 +232,16 @@ int lede_truncate(lede_ctx* ctx, int32_t new_len, void* stream);
  * lede_verify.  LEDE_E_STATE if a draft is already outstanding. */
 int lede_draft(lede_ctx* ctx, int32_t l, int32_t k, void* stream, int32_t* drafts);
 
-/* Verify the outstanding drafts (or, with none, take one autoregressive
- * step): rows [pending, d_1..d_k] at positions seq_len..seq_len+k through
- * all L layers in one pass, greedy acceptance, commit of d_1..d_a and the
- * verify token y_a, KV truncation to seq_len+a+1.  Outputs (host): accepted
- * a, tokens [k+1] (d_1..d_a, y_a), n_emitted = a+1, verify (nullable,
- * [k+1]) the full model's argmax of every row.  Synchronises. */
+/* Verify (Section 1: the full model checks the k drafts in one parallel
+ * pass; Section 4.1: greedy decoding, so a draft is kept while it equals the
+ * full model's argmax) the outstanding drafts, or, with none, take one
+ * autoregressive step: rows [pending, d_1..d_k] at positions
+ * seq_len..seq_len+k through all L layers in one pass, greedy acceptance,
+ * commit of d_1..d_a and the verify token y_a, KV truncation to seq_len+a+1.
+ * Outputs (host): accepted a, tokens [k+1] (d_1..d_a, y_a), n_emitted = a+1,
+ * verify (nullable, [k+1]) the full model's argmax of every row.  On failure
+ * the outstanding draft is discarded with the rest of the transition.
+ * LEDE_E_STATE without a pending token.  Synchronises. */
 int lede_verify(lede_ctx* ctx, void* stream, int32_t* accepted, int32_t* tokens,
                 int32_t* n_emitted, int32_t* verify);
 
@@ -368,7 +419,11 @@ int lede_dqn_act(lede_dqn* q, lede_ctx* ctx, const float* noise, void* stream);
  * transitions for 4); LEDE_E_ARG when cap_floats is too small. */
 int lede_dqn_read(lede_dqn* q, int32_t which, float* host, size_t cap_floats, int32_t* count, void* stream);
 
-/* Committed KV length, pending token and the page table (host copies). */
+/* The agent's view of the KV state between transitions (Section 3.1: the
+ * state is read at the committed length; the paper does not describe the
+ * cache's layout): committed KV length, pending token and the page table,
+ * logical page i -> pool page block_table[i] (host copies).  LEDE_E_ARG when
+ * cap < the table's length (n_table receives it). */
 int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t* block_table,
                       int32_t cap, int32_t* n_table);
 
@@ -382,6 +437,22 @@ int lede_get_kv_state(lede_ctx* ctx, int32_t* seq_len, int32_t* pending, int32_t
  * count.  Synchronises. */
 int lede_debug_read(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows,
                     void* stream);
+
+/* The next-token logits behind the last transition's decisions (Section
+ * 3.1.1: the distribution at layer l comes from the shared head over that
+ * layer's hidden state): which = LEDE_LOGITS_VERIFY, the full model's rows
+ * of the last verify or prefill head [rows][vocab] fp32; LEDE_LOGITS_DRAFT,
+ * the exit head's rows of the last step's drafts.  Needs
+ * set_options(debug = 1) (LEDE_E_STATE); LEDE_E_ARG on a bad `which` or
+ * cap_floats below rows * vocab.  Synchronises. */
+enum { LEDE_LOGITS_VERIFY = 0, LEDE_LOGITS_DRAFT = 1 };
+int lede_debug_logits(lede_ctx* ctx, int32_t which, float* host, size_t cap_floats, int32_t* rows, void* stream);
+
+/* For callers that test failure handling: the (n_ops + 1)-th device
+ * operation (kernel or graph launch, or copy) that a call on ctx issues from
+ * now on fails with LEDE_E_HIP before it is issued; one-shot; n_ops < 0
+ * disables it.  Nothing faults on the device. */
+int lede_debug_inject_failure(lede_ctx* ctx, int32_t n_ops);
 
 /* ---- timing for roofline reports ------------------------------------------
  * Level 1 brackets the draft phase and the verify phase of each lede_step
@@ -423,11 +494,14 @@ size_t lede_op_tiled_bytes(int32_t dtype, int32_t N, int32_t K);
 int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* tiled, void* stream);
 
 /* y[m][n] = sum_k W[n][k] x[m][k] (fp32 accumulate) for m < M <= 16 with a
- * tiled W (N multiple of 16) and x [M][K] in the model dtype (device).
- * use_mfma = 0 requires M = 1 (the draft path's vector kernel); 1 uses the
- * matrix-core kernel of the verify path. */
-int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M,
-                   float* y, int32_t use_mfma, void* stream);
+ * tiled W (N multiple of 16, any K) and x [M][ldx] in the model dtype
+ * (device).  The kernels read whole tiles: ldx must be at least K rounded up
+ * to the tile width (32 bf16 / 16 fp32 columns; LEDE_E_ARG otherwise) and
+ * the columns K..ldx-1 must hold finite values (they meet the tiles' zero
+ * padding).  use_mfma = 0 requires M = 1 (the draft path's vector kernel); 1
+ * uses the matrix-core kernel of the verify path. */
+int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t ldx,
+                   int32_t M, float* y, int32_t use_mfma, void* stream);
 
 /* One draw from softmax(logits / temperature) by inverse CDF in index order
  * with the uniform u in [0, 1), as the sampled step draws its drafts: logits

@@ -91,6 +91,7 @@ struct TracePushArgs {
   const int32_t* record;                           // rows = record[0] + 1 when set, else n_rows
   int n_rows;
   float* trace; int32_t* trace_state;              // state[0] = count, state[1] = next slot
+  float* backup;                                   // [POLICY_TRACE + 2]: the ring and state before the push
 };
 
 // Offline optimisation of the exit policy's Q-network (3 -> H -> 2 MLP with

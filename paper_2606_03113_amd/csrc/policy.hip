@@ -102,6 +102,11 @@ __global__ __launch_bounds__(SB) void k_exit_policy(ExitPolicyArgs a) {
 __global__ __launch_bounds__(SB) void k_trace_push(TracePushArgs a) {
   __shared__ float red[SW];
   const int n = a.record ? a.record[0] + 1 : a.n_rows;
+  // the window as it was, kept so that a failed call can be rolled back
+  static_assert(SB >= POLICY_TRACE, "one thread per slot");
+  if (threadIdx.x < POLICY_TRACE) a.backup[threadIdx.x] = a.trace[threadIdx.x];
+  if (threadIdx.x < 2) ((int32_t*)(a.backup + POLICY_TRACE))[threadIdx.x] = a.trace_state[threadIdx.x];
+  __syncthreads();
   for (int j = 0; j < n; ++j) {
     const float2 st = row_stats(a.logits + (size_t)j * a.ld, a.vocab, 1.f, red);
     if (threadIdx.x == 0) {

@@ -39,7 +39,7 @@ struct Layout {
   int He;  // exit-policy Q-network hidden width (0: none)
   // workspace offsets
   size_t h, xn, ss, q, attn_out, act, part, logits, gstats, dkeys, vkeys, qs, qhid, qv, seq_len, btab, prompt,
-      record, rope, unif, dstats, trace, trace_state, pol_out, wsbytes;
+      record, rope, unif, dstats, trace, trace_state, trace_bak, pol_out, wsbytes;
   size_t kvbytes, kv_half;
 };
 
@@ -132,6 +132,7 @@ Layout make_layout(const lede_config* c) {
   o.dstats = take(2 * SAMPLE_SLOTS * 4);
   o.trace = take(POLICY_TRACE * 4);
   o.trace_state = take(4 * 4);
+  o.trace_bak = take((POLICY_TRACE + 2) * 4);
   o.pol_out = take((size_t)(c->n_exits + POLICY_MAX_DRAFT) * POLICY_LOG * 4);
   o.wsbytes = off;
 
@@ -188,6 +189,12 @@ struct lede_ctx {
   std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
   int last_rows = 0, last_draft_rows = 0;
   std::string err;
+  // failure handling: device work issued by the current call (a failed call
+  // then restores the device's copies of the state), whether it pushed to the
+  // confidence trace, and the host-injected failure countdown
+  // (lede_debug_inject_failure; -1: none)
+  bool launched = false, trace_pushed = false;
+  int fail_after = -1;
 
   // timing (lede_prof_*): event pairs folded into per-class totals;
   // level 1 brackets the draft and verify phases, level 2 also every launch
@@ -217,6 +224,21 @@ int fail(lede_ctx* c, int code, const char* fmt, ...) {
   }
   return code;
 }
+
+// Every device operation of a call (kernel or graph launch, copy) passes
+// here first: it counts down a host-injected failure, and notes that the call
+// has touched the device.
+int pre_launch(lede_ctx* c) {
+  if (c->fail_after >= 0 && c->fail_after-- == 0)
+    return fail(c, LEDE_E_HIP, "injected failure (lede_debug_inject_failure)");
+  c->launched = true;
+  return LEDE_OK;
+}
+#define PRE()                      \
+  do {                             \
+    int rc_p_ = pre_launch(c);     \
+    if (rc_p_) return rc_p_;       \
+  } while (0)
 
 #define HIP_CHECK(ctx, expr)                                                               \
   do {                                                                                     \
@@ -275,6 +297,7 @@ int prof_fold(lede_ctx* c) {
 // events (kernel execution only).
 int launch_linear_timed(lede_ctx* c, int cls, double bytes, int dt, bool mfma, const LinearArgs& a, int grid,
                         hipStream_t s) {
+  PRE();
   if (c->prof < 2) {
     HIP_CHECK(c, launch_linear(dt, mfma, a, grid, s));
     return LEDE_OK;
@@ -307,6 +330,7 @@ int linear_class(int dt, bool vec, int K, int M) {
 #define LAUNCH(cls, bytes, expr)                         \
   do {                                                   \
     hipEvent_t e0_ = nullptr;                            \
+    PRE();                                               \
     int rc_ = prof_mark(c, s, &e0_);                     \
     if (rc_) return rc_;                                 \
     HIP_CHECK(c, (expr));                                \
@@ -370,6 +394,7 @@ int upload_table(lede_ctx* c, hipStream_t s, int32_t* stage = nullptr) {
     same = same && c->table_dev[j] == t[j];
   }
   if (same) return LEDE_OK;
+  PRE();
   HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.btab), t, n * 4, hipMemcpyHostToDevice, s));
   c->table_dev.assign(t, t + n);
   return LEDE_OK;
@@ -395,6 +420,7 @@ int wait_stream(lede_ctx* c, hipStream_t s) {
 }
 
 int upload_seq_len(lede_ctx* c, int v, hipStream_t s) {
+  PRE();
   c->record_h[RECORD_INTS - 1] = v;
   HIP_CHECK(c, hipMemcpyAsync(c->S<int32_t>(c->lo.seq_len), &c->record_h[RECORD_INTS - 1], 4, hipMemcpyHostToDevice, s));
   HIP_CHECK(c, hipStreamSynchronize(s));
@@ -476,6 +502,7 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
                uint64_t* zero_slot, hipStream_t s, int vec_row = 0) {
   const Layout& o = c->lo;
   const int dt = o.dt;
+  c->split_row = -1;
   float* hrow = c->S<float>(o.h) + (vec ? (size_t)vec_row * o.d : 0);
   for (int j = l_begin; j < l_end; ++j) {
     const auto& lw = o.lay[j];
@@ -594,7 +621,9 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       qo.w2 = c->W<float>(o.qw2); qo.b2 = c->W<float>(o.qb2); qo.A = o.A;
       qo.qv = c->S<float>(o.qv); qo.action = c->S<int32_t>(o.record) + 48;
       if (defer) {
+        PRE();
         HIP_CHECK(c, launch_linear(0, false, la, la.n_groups, qstream));
+        PRE();
         HIP_CHECK(c, launch_qnet_out(qo, qstream));
         HIP_CHECK(c, hipEventRecord(c->side_out, qstream));
         c->side_pending = 1;
@@ -604,6 +633,9 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
       }
     }
   }
+  // a one-row pass's last down projection prepared the final norm's split
+  // for its row (a multi-row pass's head reads it through its `split` flag)
+  if (vec && l_end > l_begin) c->split_row = vec_row;
   return LEDE_OK;
 }
 
@@ -686,7 +718,9 @@ int push_trace(lede_ctx* c, const float* logits, int rows, const int32_t* record
   ta.logits = logits; ta.vocab = c->lo.V; ta.ld = c->lo.V;
   ta.record = record; ta.n_rows = rows;
   ta.trace = c->S<float>(c->lo.trace); ta.trace_state = c->S<int32_t>(c->lo.trace_state);
+  ta.backup = c->S<float>(c->lo.trace_bak);
   LAUNCH(LEDE_K_ACCEPT, (double)(rows ? rows : 2) * c->lo.V * 4, launch_trace_push(ta, s));
+  c->trace_pushed = true;
   return LEDE_OK;
 }
 
@@ -710,6 +744,7 @@ int launch_verify(lede_ctx* c, int k, hipStream_t s, float inv_t = 0.f, int from
   int rc;
   if (from_layer >= c->lo.L) {
     // no layer left: the head's argmax slots are cleared here
+    PRE();
     HIP_CHECK(c, launch_fill_u64(vk, 0, KEY_WORDS, s));
   } else if ((rc = run_layers(c, k + 1, false, tok, 0, from_layer, c->lo.L, 0, vk, s))) {
     return rc;
@@ -762,6 +797,7 @@ int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
     if (ei != hipSuccess) return fail(c, LEDE_E_HIP, "hipGraphInstantiate: %s", hipGetErrorString(ei));
     it = c->graphs.emplace(key, ex).first;
   }
+  PRE();
   HIP_CHECK(c, hipGraphLaunch(it->second, s));
   if (k > 0) c->last_draft_rows = k;  // as the eager launches leave them
   c->last_rows = k + 1;
@@ -772,9 +808,68 @@ int step_graph(lede_ctx* c, int l, int k, int qa, hipStream_t s) {
 // written there by the Q-network's output kernel), in one read-back.
 int read_record(lede_ctx* c, hipStream_t s) {
   if (int rc = join_side(c, s)) return rc;
+  PRE();
   HIP_CHECK(c, hipMemcpyAsync(c->record_h, c->S<int32_t>(c->lo.record), 50 * 4, hipMemcpyDeviceToHost, s));
   return wait_stream(c, s);
 }
+
+// Restore the decoding state a failed call started from: committed length
+// c0, pending token pending0, the page table of c0 positions (pages freed by
+// truncate_pages go back to the front of the free list in logical order, so
+// re-taking them rebuilds the same table), no outstanding draft.  When the
+// call had issued device work, the device's copies (length, pending token,
+// table, confidence trace) are rewritten after the stream drains.  Keeps the
+// error text of the original failure; best effort when the device itself
+// has failed.
+void rollback(lede_ctx* c, hipStream_t s, int c0, int pending0) {
+  const std::string keep = c->err;
+  c->fail_after = -1;
+  truncate_pages(c, c0);
+  (void)ensure_pages(c, c0);
+  c->seq_len = c0;
+  c->pending = pending0;
+  c->drafted_k = -1;
+  c->policy_valid = 0;
+  c->split_row = -1;
+  if (c->launched) {
+    (void)hipStreamSynchronize(s);
+    (void)hipStreamSynchronize(c->side);
+    c->side_pending = 0;
+    c->table_dev.assign(c->lo.max_pages_seq, -3);  // not a value the host ever uploads
+    (void)upload_table(c, s);
+    (void)upload_seq_len(c, c0, s);
+    if (pending0 >= 0) (void)launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, pending0, s);
+    if (c->trace_pushed) {
+      (void)hipMemcpyAsync(c->S<float>(c->lo.trace), c->S<float>(c->lo.trace_bak), POLICY_TRACE * 4,
+                           hipMemcpyDeviceToDevice, s);
+      (void)hipMemcpyAsync(c->S<int32_t>(c->lo.trace_state), c->S<float>(c->lo.trace_bak) + POLICY_TRACE, 2 * 4,
+                           hipMemcpyDeviceToDevice, s);
+    }
+    (void)hipStreamSynchronize(s);
+  }
+  c->launched = c->trace_pushed = false;
+  c->err = keep;
+}
+
+// A call that changes the decoding state: when it fails after it has
+// allocated pages or issued device work (or always, with force), the state
+// it started from is restored (rollback).  A failed argument or state check
+// changes nothing.
+struct Txn {
+  lede_ctx* c;
+  hipStream_t s;
+  int c0, pending0;
+  size_t n_table0;
+  bool force;
+  Txn(lede_ctx* c_, hipStream_t s_, bool force_ = false)
+      : c(c_), s(s_), c0(c_->seq_len), pending0(c_->pending), n_table0(c_->table.size()), force(force_) {
+    c->launched = c->trace_pushed = false;
+  }
+  int done(int rc) {
+    if (rc != LEDE_OK && (force || c->launched || c->table.size() != n_table0)) rollback(c, s, c0, pending0);
+    return rc;
+  }
+};
 
 // Apply a finished verify (record read back) to the host mirror.
 void commit_host(lede_ctx* c) {
@@ -954,9 +1049,57 @@ int lede_set_free_list(lede_ctx* c, const int32_t* order, int32_t n) {
 int lede_set_options(lede_ctx* c, int32_t use_graphs, int32_t debug) {
   if (!c) return LEDE_E_ARG;
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
+  // a captured step keeps the logits pointers of the debug mode it was
+  // captured in: a change of either option drops the captures
+  if ((debug != 0) != (c->debug != 0) || (use_graphs != 0) != (c->use_graphs != 0)) {
+    for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.second);
+    c->graphs.clear();
+  }
   c->use_graphs = use_graphs;
   c->debug = debug;
   return LEDE_OK;
+}
+
+int lede_debug_inject_failure(lede_ctx* c, int32_t n_ops) {
+  if (!c) return LEDE_E_ARG;
+  c->fail_after = n_ops < 0 ? -1 : n_ops;
+  return LEDE_OK;
+}
+
+int lede_load_weights(lede_ctx* c, const lede_weights* w, void* stream) {
+  if (!c || !w) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
+  const Layout& o = c->lo;
+  if (w->n_layers < 0 || w->first_layer < 0 || w->first_layer + w->n_layers > o.L)
+    return fail(c, LEDE_E_ARG, "layers [%d, %d) outside the model's %d", w->first_layer,
+                w->first_layer + w->n_layers, o.L);
+  if (w->n_layers > 0 && !w->layer) return fail(c, LEDE_E_ARG, "null layer table");
+  if (!o.H && (w->qnet_w1 || w->qnet_b1 || w->qnet_w2 || w->qnet_b2))
+    return fail(c, LEDE_E_STATE, "config has no Q-network");
+  if (!o.He && (w->exit_w1 || w->exit_b1 || w->exit_w2 || w->exit_b2))
+    return fail(c, LEDE_E_STATE, "config has no exit policy");
+  // every tensor named is repacked or copied in order; a null entry is left as it is
+  struct Item { int kind, layer; const void* src; };
+  std::vector<Item> items = {{LEDE_T_EMBED, 0, w->embed}, {LEDE_T_FINAL_NORM, 0, w->final_norm},
+                             {LEDE_T_HEAD, 0, w->head}};
+  for (int j = 0; j < w->n_layers; ++j)
+    for (int t = 0; t < LEDE_LAYER_TENSORS; ++t)
+      items.push_back({LEDE_T_ATTN_NORM + t, w->first_layer + j, w->layer[(size_t)j * LEDE_LAYER_TENSORS + t]});
+  const void* rest[8] = {w->qnet_w1, w->qnet_b1, w->qnet_w2, w->qnet_b2, w->exit_w1, w->exit_b1, w->exit_w2, w->exit_b2};
+  for (int t = 0; t < 8; ++t) items.push_back({LEDE_T_QNET_W1 + t, 0, rest[t]});
+  for (const Item& it : items) {
+    if (!it.src) continue;
+    const int rc = lede_load_tensor(c, it.kind, it.layer, it.src, stream);
+    if (rc) return rc;
+  }
+  return LEDE_OK;
+}
+
+int lede_debug_logits(lede_ctx* c, int32_t which, float* host, size_t cap_floats, int32_t* rows, void* stream) {
+  if (!c) return LEDE_E_ARG;
+  if (which != LEDE_LOGITS_VERIFY && which != LEDE_LOGITS_DRAFT)
+    return fail(c, LEDE_E_ARG, "which must be LEDE_LOGITS_VERIFY or LEDE_LOGITS_DRAFT");
+  return lede_debug_read(c, which == LEDE_LOGITS_VERIFY ? 0 : 3, host, cap_floats, rows, stream);
 }
 
 int lede_set_verify_reuse(lede_ctx* c, int32_t enable) {
@@ -967,6 +1110,43 @@ int lede_set_verify_reuse(lede_ctx* c, int32_t enable) {
   return LEDE_OK;
 }
 
+static int prefill_impl(lede_ctx* c, const int32_t* tokens, int32_t n, hipStream_t s, int32_t* next_token) {
+  c->policy_valid = 0;
+  const int c0 = c->seq_len;
+  int rc = ensure_pages(c, c0 + n);
+  if (rc) return rc;
+  if ((rc = upload_table(c, s)) || (rc = upload_seq_len(c, c0, s))) return rc;
+  int32_t* pd = c->S<int32_t>(c->lo.prompt);
+  PRE();
+  HIP_CHECK(c, hipMemcpyAsync(pd, tokens, (size_t)n * 4, hipMemcpyHostToDevice, s));
+  uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
+  int last_m = 0;
+  for (int off = 0; off < n; off += MROWS) {
+    const int M = std::min(MROWS, n - off);
+    TokenSrc tok{pd + off, nullptr};
+    if ((rc = run_layers(c, M, false, tok, off, 0, c->lo.L, 0, vk, s))) return rc;
+    if (off + M == n) {
+      const bool trace = c->lo.He > 0;
+      if ((rc = run_head(c, M, false, vk, verify_logits(c, trace), s, 0, true))) return rc;
+      if (trace && (rc = push_trace(c, verify_logits(c, true) + (size_t)(M - 1) * c->lo.V, 1, nullptr, s)))
+        return rc;
+    }
+    last_m = M;
+  }
+  c->last_rows = last_m;
+  PRE();
+  HIP_CHECK(c, hipMemcpyAsync(c->keys_h, vk, KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
+  HIP_CHECK(c, hipStreamSynchronize(s));
+  const int next = key_token(key_value(c->keys_h, last_m - 1));
+  PRE();
+  HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, next, s));
+  if ((rc = upload_seq_len(c, c0 + n, s))) return rc;
+  c->seq_len = c0 + n;
+  c->pending = next;
+  if (next_token) *next_token = next;
+  return LEDE_OK;
+}
+
 int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, int32_t* next_token) {
   if (!c || !tokens || n < 1) return fail(c, LEDE_E_ARG, "bad prefill arguments");
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
@@ -974,42 +1154,8 @@ int lede_prefill(lede_ctx* c, const int32_t* tokens, int32_t n, void* stream, in
   for (int i = 0; i < n; ++i)
     if (tokens[i] < 0 || tokens[i] >= c->lo.V) return fail(c, LEDE_E_ARG, "token %d out of range", tokens[i]);
   hipStream_t s = S_(stream);
-  c->policy_valid = 0;
-  const int c0 = c->seq_len;
-  const size_t saved_table = c->table.size();
-  int rc = ensure_pages(c, c0 + n);
-  if (rc) return rc;
-  if ((rc = upload_table(c, s)) || (rc = upload_seq_len(c, c0, s))) { truncate_pages(c, c0); return rc; }
-  int32_t* pd = c->S<int32_t>(c->lo.prompt);
-  if (hipMemcpyAsync(pd, tokens, (size_t)n * 4, hipMemcpyHostToDevice, s) != hipSuccess) {
-    truncate_pages(c, c0);
-    return fail(c, LEDE_E_HIP, "prompt upload failed");
-  }
-  uint64_t* vk = c->S<uint64_t>(c->lo.vkeys);
-  int last_m = 0;
-  for (int off = 0; off < n; off += MROWS) {
-    const int M = std::min(MROWS, n - off);
-    TokenSrc tok{pd + off, nullptr};
-    rc = run_layers(c, M, false, tok, off, 0, c->lo.L, 0, vk, s);
-    if (!rc && off + M == n) {
-      const bool trace = c->lo.He > 0;
-      rc = run_head(c, M, false, vk, verify_logits(c, trace), s, 0, true);
-      if (!rc && trace) rc = push_trace(c, verify_logits(c, true) + (size_t)(M - 1) * c->lo.V, 1, nullptr, s);
-    }
-    if (rc) { truncate_pages(c, c0); (void)saved_table; return rc; }
-    last_m = M;
-  }
-  c->last_rows = last_m;
-  HIP_CHECK(c, hipMemcpyAsync(c->keys_h, vk, KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
-  HIP_CHECK(c, hipStreamSynchronize(s));
-  const int next = key_token(key_value(c->keys_h, last_m - 1));
-  HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, next, s));
-  rc = upload_seq_len(c, c0 + n, s);
-  if (rc) return rc;
-  c->seq_len = c0 + n;
-  c->pending = next;
-  if (next_token) *next_token = next;
-  return LEDE_OK;
+  Txn t(c, s);
+  return t.done(prefill_impl(c, tokens, n, s, next_token));
 }
 
 int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
@@ -1018,11 +1164,14 @@ int lede_set_pending(lede_ctx* c, int32_t token, void* stream) {
   if (token < 0 || token >= c->lo.V) return fail(c, LEDE_E_ARG, "token out of range");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
   hipStream_t s = S_(stream);
+  Txn t(c, s);
   c->policy_valid = 0;
-  HIP_CHECK(c, launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, token, s));
-  HIP_CHECK(c, hipStreamSynchronize(s));
-  c->pending = token;
-  return LEDE_OK;
+  int rc = pre_launch(c);
+  if (!rc && launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, token, s) != hipSuccess)
+    rc = fail(c, LEDE_E_HIP, "launch_set_token failed");
+  if (!rc && hipStreamSynchronize(s) != hipSuccess) rc = fail(c, LEDE_E_HIP, "hipStreamSynchronize failed");
+  if (!rc) c->pending = token;
+  return t.done(rc);
 }
 
 int lede_truncate(lede_ctx* c, int32_t new_len, void* stream) {
@@ -1030,15 +1179,15 @@ int lede_truncate(lede_ctx* c, int32_t new_len, void* stream) {
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (new_len < 0 || new_len > c->seq_len) return fail(c, LEDE_E_ARG, "new_len %d not in [0, %d]", new_len, c->seq_len);
   hipStream_t s = S_(stream);
+  // a failed truncation leaves the state as it was, outstanding draft aside
+  Txn t(c, s);
   c->policy_valid = 0;
   truncate_pages(c, new_len);
   c->drafted_k = -1;
   int rc = upload_table(c, s);
-  if (rc) return rc;
-  rc = upload_seq_len(c, new_len, s);
-  if (rc) return rc;
-  c->seq_len = new_len;
-  return LEDE_OK;
+  if (!rc) rc = upload_seq_len(c, new_len, s);
+  if (!rc) c->seq_len = new_len;
+  return t.done(rc);
 }
 
 static int draft_impl(lede_ctx* c, int l, int k, hipStream_t s) {
@@ -1046,10 +1195,9 @@ static int draft_impl(lede_ctx* c, int l, int k, hipStream_t s) {
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
   if (l < 1 || l > c->lo.L) return fail(c, LEDE_E_ARG, "exit layer %d not in 1..%d", l, c->lo.L);
   if (k < 1 || k > c->lo.k_max) return fail(c, LEDE_E_ARG, "draft length %d not in 1..%d", k, c->lo.k_max);
-  const size_t before = c->table.size();
   int rc = ensure_pages(c, c->seq_len + k + 1);
   if (rc) return rc;
-  if ((rc = upload_table(c, s))) { truncate_pages(c, c->seq_len); (void)before; return rc; }
+  if ((rc = upload_table(c, s))) return rc;
   rc = launch_drafts(c, l, 1, k, 0, 0, s);
   if (rc) return rc;
   c->drafted_k = k;
@@ -1061,14 +1209,46 @@ int lede_draft(lede_ctx* c, int32_t l, int32_t k, void* stream, int32_t* drafts)
   if (!c) return LEDE_E_ARG;
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   hipStream_t s = S_(stream);
+  Txn t(c, s);
   int rc = draft_impl(c, l, k, s);
-  if (rc) return rc;
+  if (rc) return t.done(rc);
   c->policy_valid = 0;
   if (drafts) {
-    HIP_CHECK(c, hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
-    HIP_CHECK(c, hipStreamSynchronize(s));
+    rc = pre_launch(c);
+    if (!rc && (hipMemcpyAsync(c->keys_h, c->S<uint64_t>(c->lo.dkeys), KEY_WORDS * 8, hipMemcpyDeviceToHost, s) !=
+                    hipSuccess ||
+                hipStreamSynchronize(s) != hipSuccess))
+      rc = fail(c, LEDE_E_HIP, "draft read-back failed");
+    if (rc) return t.done(rc);
     for (int i = 0; i < k; ++i) drafts[i] = key_token(key_value(c->keys_h, i + 1));
   }
+  return LEDE_OK;
+}
+
+static int verify_impl(lede_ctx* c, hipStream_t s, int32_t* accepted, int32_t* tokens, int32_t* n_emitted,
+                       int32_t* verify) {
+  const int k = c->drafted_k < 0 ? 0 : c->drafted_k;
+  int rc;
+  if (c->drafted_k < 0) {
+    if ((rc = ensure_pages(c, c->seq_len + 1))) return rc;
+    if ((rc = upload_table(c, s))) return rc;
+  }
+  const int from = (c->verify_reuse && k > 0) ? c->drafted_l : 0;
+  rc = from ? extend_drafts(c, from, k, s) : LEDE_OK;
+  if (!rc) rc = launch_verify(c, k, s, 0.f, from);
+  if (rc) return rc;
+  if (verify) {
+    PRE();
+    HIP_CHECK(c, hipMemcpyAsync(c->keys_h + KEY_WORDS, c->S<uint64_t>(c->lo.vkeys), KEY_WORDS * 8,
+                                hipMemcpyDeviceToHost, s));
+  }
+  if ((rc = read_record(c, s))) return rc;
+  commit_host(c);
+  const int a = c->record_h[0];
+  if (accepted) *accepted = a;
+  if (n_emitted) *n_emitted = a + 1;
+  if (tokens) for (int i = 0; i <= a; ++i) tokens[i] = c->record_h[4 + i];
+  if (verify) for (int i = 0; i <= k; ++i) verify[i] = key_token(key_value(c->keys_h + KEY_WORDS, i));
   return LEDE_OK;
 }
 
@@ -1077,27 +1257,10 @@ int lede_verify(lede_ctx* c, void* stream, int32_t* accepted, int32_t* tokens, i
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
   if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
   hipStream_t s = S_(stream);
-  const int k = c->drafted_k < 0 ? 0 : c->drafted_k;
-  if (c->drafted_k < 0) {
-    int rc = ensure_pages(c, c->seq_len + 1);
-    if (rc) return rc;
-    if ((rc = upload_table(c, s))) return rc;
-  }
-  const int from = (c->verify_reuse && k > 0) ? c->drafted_l : 0;
-  int rc = from ? extend_drafts(c, from, k, s) : LEDE_OK;
-  if (!rc) rc = launch_verify(c, k, s, 0.f, from);
-  if (rc) return rc;
-  if (verify)
-    HIP_CHECK(c, hipMemcpyAsync(c->keys_h + KEY_WORDS, c->S<uint64_t>(c->lo.vkeys), KEY_WORDS * 8, hipMemcpyDeviceToHost, s));
-  rc = read_record(c, s);
-  if (rc) return rc;
-  commit_host(c);
-  const int a = c->record_h[0];
-  if (accepted) *accepted = a;
-  if (n_emitted) *n_emitted = a + 1;
-  if (tokens) for (int i = 0; i <= a; ++i) tokens[i] = c->record_h[4 + i];
-  if (verify) for (int i = 0; i <= k; ++i) verify[i] = key_token(key_value(c->keys_h + KEY_WORDS, i));
-  return LEDE_OK;
+  // a failed verify also discards the outstanding draft: the transition
+  // (draft, verify, commit) rolls back to the committed state it started from
+  Txn t(c, s, true);
+  return t.done(verify_impl(c, s, accepted, tokens, n_emitted, verify));
 }
 
 }  // extern "C"
@@ -1134,7 +1297,7 @@ void fill_record(const lede_ctx* c, const int32_t* r, int l, int k, int k_eff, b
   }
 }
 
-int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, float temperature,
+int step_body(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, float temperature,
               const float* uniforms, void* stream, lede_step_record* rec) {
   if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
   if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
@@ -1164,6 +1327,7 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   }
   if (sampled) {
     memcpy(c->unif_h, uniforms, UNIF_FLOATS * 4);
+    PRE();
     HIP_CHECK(c, hipMemcpyAsync(c->S<float>(o.unif), c->unif_h, UNIF_FLOATS * 4, hipMemcpyHostToDevice, s));
   }
   const int l_min = o.H ? c->cfg.exits[0] : 0;
@@ -1182,6 +1346,7 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       uint64_t* dk = c->S<uint64_t>(o.dkeys);
       rc = run_layers(c, 1, true, TokenSrc{nullptr, dk}, 0, 0, l_min, l_min, dk + 1, s);
       if (rc) return rc;
+      PRE();
       HIP_CHECK(c, hipMemcpyAsync(c->record_h + 48, c->S<int32_t>(o.record) + 48, 2 * 4, hipMemcpyDeviceToHost, s));
       if ((rc = wait_stream(c, s))) return rc;
       const int a = c->record_h[48];
@@ -1190,18 +1355,18 @@ int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
       k = c->cfg.lengths[a % c->cfg.n_lengths];
       k_eff = std::min(std::min(k, o.k_max), n_remaining - 1);
       ran_q = true;
-      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) return rc;
       rc = launch_drafts(c, l, 1, k_eff, 0, l_min, s, inv_t);
       if (rc) return rc;
     } else {
-      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+      if ((rc = ensure_pages(c, c0 + k_eff + 1)) || (rc = upload_table(c, s))) return rc;
       const int qa = (want_q && l_min <= l) ? l_min : 0;
       ran_q = qa > 0;
       if (c->use_graphs && !c->prof && s && !sampled && !c->verify_reuse) {
         // the whole step as one graph: every launch reads positions, tokens
         // and pages from device memory, so a capture serves every step of
         // the same shape
-        if ((rc = step_graph(c, l, k_eff, qa, s))) { truncate_pages(c, c0); return rc; }
+        if ((rc = step_graph(c, l, k_eff, qa, s))) return rc;
         goto verified;
       }
       c->qnet_defer = 1;
@@ -1236,6 +1401,13 @@ verified:
   return LEDE_OK;
 }
 
+int step_impl(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t n_remaining, float temperature,
+              const float* uniforms, void* stream, lede_step_record* rec) {
+  if (!c) return LEDE_E_ARG;
+  Txn t(c, S_(stream));
+  return t.done(step_body(c, forced, log_qnet, n_remaining, temperature, uniforms, stream, rec));
+}
+
 }  // namespace
 
 extern "C" {
@@ -1245,7 +1417,51 @@ int lede_step(lede_ctx* c, const lede_action* forced, int32_t log_qnet, int32_t 
   return step_impl(c, forced, log_qnet, n_remaining, 0.f, nullptr, stream, rec);
 }
 
+static int submit_body(lede_ctx* c, const lede_action* action, int32_t log_qnet, int32_t n_remaining,
+                       void* stream);
+
+// A failed submit: the steps in flight before it stay queued; the pages and
+// the device's copies of the state return to what those steps leave (their
+// records have arrived once the stream has drained).
+static void submit_rollback(lede_ctx* c, hipStream_t s, int ub_prev) {
+  const std::string keep = c->err;
+  c->fail_after = -1;
+  truncate_pages(c, ub_prev);
+  (void)ensure_pages(c, ub_prev);
+  c->policy_valid = 0;
+  c->split_row = -1;
+  if (c->launched) {
+    (void)hipStreamSynchronize(s);
+    (void)hipStreamSynchronize(c->side);
+    c->side_pending = 0;
+    int len = c->seq_len, pend = c->pending;
+    if (!c->inflight.empty()) {
+      const int32_t* r = c->rec_slots_h + (size_t)c->inflight.back().slot * RECORD_INTS;
+      len = r[2];
+      pend = r[3];
+    }
+    c->table_dev.assign(c->lo.max_pages_seq, -3);
+    (void)upload_table(c, s);
+    (void)upload_seq_len(c, len, s);
+    (void)launch_set_token(c->S<uint64_t>(c->lo.dkeys), 0, pend, s);
+    (void)hipStreamSynchronize(s);
+  }
+  c->launched = c->trace_pushed = false;
+  c->err = keep;
+}
+
 int lede_step_submit(lede_ctx* c, const lede_action* action, int32_t log_qnet, int32_t n_remaining, void* stream) {
+  if (!c) return LEDE_E_ARG;
+  const int ub_prev = c->inflight.empty() ? c->seq_len : c->seq_ub;
+  const size_t n_table0 = c->table.size();
+  c->launched = c->trace_pushed = false;
+  const int rc = submit_body(c, action, log_qnet, n_remaining, stream);
+  if (rc != LEDE_OK && (c->launched || c->table.size() != n_table0)) submit_rollback(c, S_(stream), ub_prev);
+  return rc;
+}
+
+static int submit_body(lede_ctx* c, const lede_action* action, int32_t log_qnet, int32_t n_remaining,
+                       void* stream) {
   if (!c || !action) return fail(c, LEDE_E_ARG, "null argument");
   if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
   if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
@@ -1284,10 +1500,11 @@ int lede_step_submit(lede_ctx* c, const lede_action* action, int32_t log_qnet, i
   if (rc) return rc;
   if ((rc = launch_verify(c, k_eff, s))) return rc;
   if ((rc = join_side(c, s))) return rc;
-  c->next_slot = (slot + 1) % LEDE_MAX_IN_FLIGHT;
+  PRE();
   HIP_CHECK(c, hipMemcpyAsync(c->rec_slots_h + (size_t)slot * RECORD_INTS, c->S<int32_t>(o.record), 50 * 4,
                               hipMemcpyDeviceToHost, s));
   HIP_CHECK(c, hipEventRecord(c->rec_ev[slot], s));
+  c->next_slot = (slot + 1) % LEDE_MAX_IN_FLIGHT;
   c->inflight.push_back(lede_ctx::InFlight{l, k, k_eff, slot, qa > 0});
   c->seq_ub = ub + k_eff + 1;
   c->pipe_stream = stream;
@@ -1319,15 +1536,8 @@ int lede_step_sampled(lede_ctx* c, const lede_action* forced, int32_t log_qnet, 
   return step_impl(c, forced, log_qnet, n_remaining, temperature, uniforms, stream, rec);
 }
 
-int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_record* rec) {
-  if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
-  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
-  if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
-  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
-  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+static int policy_body(lede_ctx* c, int32_t n_remaining, hipStream_t s, lede_step_record* rec) {
   const Layout& o = c->lo;
-  if (!o.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
-  hipStream_t s = S_(stream);
   memset(rec, 0, sizeof *rec);
   rec->q_action = -1;
   rec->q_max = NAN;
@@ -1336,7 +1546,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
   const int c0 = c->seq_len;
   const int k_lim = std::max(0, std::min(std::min(POLICY_MAX_DRAFT, o.k_max), n_remaining - 1));
   int rc;
-  if ((rc = ensure_pages(c, c0 + k_lim + 1)) || (rc = upload_table(c, s))) { truncate_pages(c, c0); return rc; }
+  if ((rc = ensure_pages(c, c0 + k_lim + 1)) || (rc = upload_table(c, s))) return rc;
   uint64_t* dk = c->S<uint64_t>(o.dkeys);
   ExitPolicyArgs pa{};
   pa.vocab = o.V; pa.hidden = o.He;
@@ -1348,7 +1558,9 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
   auto decide = [&](const float* logits, int kind, int index, int* action) -> int {
     pa.out = log_dev + c->policy_log.size();
     pa.logits = logits; pa.kind = (float)kind; pa.index = (float)index;
+    PRE();
     HIP_CHECK(c, launch_exit_policy(pa, s));
+    PRE();
     HIP_CHECK(c, hipMemcpyAsync(c->trace_h, pa.out, POLICY_LOG * 4, hipMemcpyDeviceToHost, s));
     if (int rc = wait_stream(c, s)) return rc;
     c->policy_log.insert(c->policy_log.end(), c->trace_h, c->trace_h + POLICY_LOG);
@@ -1366,7 +1578,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
       if (!rc) rc = run_head(c, 1, true, dk + 1, draft_logits(c, 0, true), s);
       int act = 0;
       if (!rc) rc = decide(draft_logits(c, 0, true), 0, l, &act);
-      if (rc) { truncate_pages(c, c0); return rc; }
+      if (rc) return rc;
       begin = l;
       if (act == 1 || e == c->cfg.n_exits - 1) {
         l_star = l;
@@ -1380,7 +1592,7 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
       if (!rc) rc = run_head(c, 1, true, dk + k + 1, draft_logits(c, k, true), s, k);
       int act = 0;
       if (!rc) rc = decide(draft_logits(c, k, true), 1, k + 1, &act);
-      if (rc) { truncate_pages(c, c0); return rc; }
+      if (rc) return rc;
       ran_last = act != 1;  // 'continue': this pass was the last draft's input pass
       if (act != 1) break;
       ++k;
@@ -1411,6 +1623,20 @@ int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_r
     rec->reward = (float)(a * (1.0 + lam) + (a < k ? (-2.0 + lam) : 0.0));
   }
   return LEDE_OK;
+}
+
+int lede_step_policy(lede_ctx* c, int32_t n_remaining, void* stream, lede_step_record* rec) {
+  if (!c || !rec) return fail(c, LEDE_E_ARG, "null argument");
+  if (!c->inflight.empty()) return fail(c, LEDE_E_STATE, "pipelined steps are outstanding");
+  if (n_remaining < 1) return fail(c, LEDE_E_ARG, "n_remaining must be >= 1");
+  if (c->drafted_k >= 0) return fail(c, LEDE_E_STATE, "a draft is outstanding");
+  if (c->pending < 0) return fail(c, LEDE_E_STATE, "no pending token (prefill first)");
+  if (!c->lo.He) return fail(c, LEDE_E_STATE, "no exit policy configured");
+  hipStream_t s = S_(stream);
+  Txn t(c, s);
+  const int rc = t.done(policy_body(c, n_remaining, s, rec));
+  if (rc) c->policy_log.clear();
+  return rc;
 }
 
 int lede_set_trace(lede_ctx* c, const float* values, int32_t n, void* stream) {
@@ -1544,15 +1770,17 @@ int lede_op_repack(int32_t dtype, const void* src, int32_t N, int32_t K, void* t
   return launch_repack(dtype, ra, S_(stream)) == hipSuccess ? LEDE_OK : LEDE_E_HIP;
 }
 
-int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t M, float* y,
-                   int32_t use_mfma, void* stream) {
+int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const void* x, int32_t ldx, int32_t M,
+                   float* y, int32_t use_mfma, void* stream) {
   if ((dtype != 0 && dtype != 1) || !tiled || !x || !y || N < 1 || K < 1) return LEDE_E_ARG;
-  if (N % 16 || K % tile_k(dtype)) return LEDE_E_UNSUPPORTED;
+  if (N % 16) return LEDE_E_UNSUPPORTED;
   if (M < 1 || M > 16 || (!use_mfma && M != 1)) return LEDE_E_ARG;
+  // the kernels read whole tiles of every row: rows padded to the tile width
+  if (ldx < k_tiles(dtype, K) * tile_k(dtype)) return LEDE_E_ARG;
   LinearArgs a{};
   a.w = (const uint8_t*)tiled;
   a.n_groups = N / 16; a.KT = k_tiles(dtype, K); a.K = K; a.M = M;
-  a.x_mode = X_PLAIN; a.x = x; a.ldx = K;
+  a.x_mode = X_PLAIN; a.x = x; a.ldx = ldx;
   a.epi = EPI_STORE; a.out = y; a.ldo = N;
   return launch_linear(dtype, use_mfma != 0, a, std::min(a.n_groups, 4096), S_(stream)) == hipSuccess ? LEDE_OK
                                                                                                   : LEDE_E_HIP;

@@ -50,6 +50,20 @@ K_SYMBOLS = {"linear_vec": "lede::k_linear<1, 0>", "linear_mfma": "lede::k_linea
              "linear_vec_gx": "lede::k_linear<1, 1>", "linear_mfma_lx": "lede::k_linear<1, 3>"}
 
 
+LAYER_TENSORS = 9  # LEDE_LAYER_TENSORS: attn_norm, wq, wk, wv, wo, ffn_norm, wg, wu, wd
+LAYER_ORDER = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd"]
+LOGITS_VERIFY, LOGITS_DRAFT = 0, 1
+
+
+class LedeWeights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p), ("head", ctypes.c_void_p),
+                ("first_layer", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("layer", ctypes.POINTER(ctypes.c_void_p)),
+                ("qnet_w1", ctypes.c_void_p), ("qnet_b1", ctypes.c_void_p), ("qnet_w2", ctypes.c_void_p),
+                ("qnet_b2", ctypes.c_void_p), ("exit_w1", ctypes.c_void_p), ("exit_b1", ctypes.c_void_p),
+                ("exit_w2", ctypes.c_void_p), ("exit_b2", ctypes.c_void_p)]
+
+
 class LedeAction(ctypes.Structure):
     _fields_ = [("l", ctypes.c_int32), ("k", ctypes.c_int32)]
 
@@ -69,7 +83,7 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_get_trace", "lede_set_verify_reuse", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
             "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
             "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read", "lede_step_submit",
-            "lede_step_collect"]
+            "lede_step_collect", "lede_load_weights", "lede_debug_logits", "lede_debug_inject_failure"]
 MAX_IN_FLIGHT = 2
 SAMPLE_SLOTS = 16
 SAMPLE_STRIDE = 33
@@ -94,6 +108,9 @@ def load(path: str = LIB_PATH):
     L.lede_last_error.argtypes = [vp]
     L.lede_last_error.restype = ctypes.c_char_p
     L.lede_load_tensor.argtypes = [vp, i32, i32, vp, vp]
+    L.lede_load_weights.argtypes = [vp, P(LedeWeights), vp]
+    L.lede_debug_logits.argtypes = [vp, i32, P(ctypes.c_float), sz, P(i32), vp]
+    L.lede_debug_inject_failure.argtypes = [vp, i32]
     L.lede_set_free_list.argtypes = [vp, P(i32), i32]
     L.lede_set_options.argtypes = [vp, i32, i32]
     L.lede_set_verify_reuse.argtypes = [vp, i32]
@@ -112,7 +129,7 @@ def load(path: str = LIB_PATH):
     L.lede_op_tiled_bytes.argtypes = [i32, i32, i32]
     L.lede_op_tiled_bytes.restype = sz
     L.lede_op_repack.argtypes = [i32, vp, i32, i32, vp, vp]
-    L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, vp, i32, vp]
+    L.lede_op_linear.argtypes = [i32, vp, i32, i32, vp, i32, i32, vp, i32, vp]
     L.lede_op_read_probe.argtypes = [vp, sz, vp, i32, vp, P(ctypes.c_float)]
     L.lede_op_read_groups.argtypes = [vp, i32, i32, vp, vp, P(ctypes.c_float)]
     L.lede_step_sampled.argtypes = [vp, P(LedeAction), i32, i32, ctypes.c_float, P(ctypes.c_float), vp,
@@ -256,17 +273,60 @@ class Engine:
         self._check(self.L.lede_load_tensor(self.ctx, kind, layer, dev.data_ptr(), self.stream), self.ctx)
         t.cuda.current_stream(self.device).synchronize()
 
-    def load_weights(self, weights: dict, qnet: Optional[dict] = None):
-        """weights: lede_inputs.weights() layout; qnet: lede_inputs.qnet_weights()."""
-        self.load_tensor(T_EMBED, 0, weights["embed"])
-        self.load_tensor(T_FINAL_NORM, 0, weights["final_norm"])
-        self.load_tensor(T_HEAD, 0, weights["head"])
-        for j, lw in enumerate(weights["layers"]):
-            for name, kind in LAYER_KINDS.items():
-                self.load_tensor(kind, j, lw[name])
+    def _dev(self, host: np.ndarray):
+        a = np.ascontiguousarray(host)
+        if a.dtype == np.uint16:
+            a = a.view(np.int16)
+        return self.torch.from_numpy(a).to(self.device)
+
+    def lede_load_weights(self, weights: Optional[dict] = None, qnet: Optional[dict] = None,
+                          exit_qnet: Optional[dict] = None, first_layer: int = 0, n_layers: int = 0):
+        """One lede_load_weights call: the tensors given (host arrays in the
+        lede_inputs.weights() layout) are staged on the device and repacked;
+        absent ones are left as they are.  Layers [first_layer, first_layer +
+        n_layers) come from weights["layers"]."""
+        keep = []
+
+        def ptr(host):
+            if host is None:
+                return None
+            d = self._dev(host)
+            keep.append(d)
+            return d.data_ptr()
+
+        w = LedeWeights()
+        weights = weights or {}
+        w.embed, w.final_norm, w.head = (ptr(weights.get(n)) for n in ("embed", "final_norm", "head"))
+        w.first_layer, w.n_layers = first_layer, n_layers
+        table = (ctypes.c_void_p * max(1, n_layers * LAYER_TENSORS))()
+        layers = weights.get("layers", [])
+        for j in range(n_layers):
+            if first_layer + j >= len(layers):
+                break  # the library checks the range against the model
+            for t, name in enumerate(LAYER_ORDER):
+                table[j * LAYER_TENSORS + t] = ptr(layers[first_layer + j][name])
+        w.layer = ctypes.cast(table, ctypes.POINTER(ctypes.c_void_p))
+        f32 = lambda a: None if a is None else ptr(np.ascontiguousarray(a, dtype=np.float32))  # noqa: E731
         if qnet is not None:
-            for name, kind in (("w1", T_QNET_W1), ("b1", T_QNET_B1), ("w2", T_QNET_W2), ("b2", T_QNET_B2)):
-                self.load_tensor(kind, 0, qnet[name])
+            w.qnet_w1, w.qnet_b1, w.qnet_w2, w.qnet_b2 = (f32(qnet[n]) for n in ("w1", "b1", "w2", "b2"))
+        if exit_qnet is not None:
+            w.exit_w1, w.exit_b1, w.exit_w2, w.exit_b2 = (f32(exit_qnet[n]) for n in ("w1", "b1", "w2", "b2"))
+        self._check(self.L.lede_load_weights(self.ctx, ctypes.byref(w), self.stream), self.ctx)
+        self.torch.cuda.current_stream(self.device).synchronize()
+        del keep
+
+    def load_weights(self, weights: dict, qnet: Optional[dict] = None, staging_bytes: int = 16 << 30):
+        """weights: lede_inputs.weights() layout; qnet: lede_inputs.qnet_weights().
+        Through lede_load_weights: the embedding, head and Q-network in one
+        call, then the layers in groups whose staging copies take at most
+        staging_bytes of device memory."""
+        self.lede_load_weights({n: weights[n] for n in ("embed", "final_norm", "head")}, qnet)
+        layers = weights["layers"]
+        per_layer = max(1, sum(np.asarray(a).nbytes for a in layers[0].values())) if layers else 1
+        group = max(1, staging_bytes // per_layer)
+        for j0 in range(0, len(layers), group):
+            n = min(group, len(layers) - j0)
+            self.lede_load_weights({"layers": layers}, first_layer=j0, n_layers=n)
 
     # -- C-ABI calls (same names) --------------------------------------------------
     def lede_set_options(self, use_graphs: int = 0, debug: int = 0):
@@ -347,8 +407,7 @@ class Engine:
 
     def load_exit_qnet(self, w: dict):
         """The exit policy's Q-network: lede_inputs.exit_qnet_weights() layout."""
-        for kind, name in ((T_EXIT_W1, "w1"), (T_EXIT_B1, "b1"), (T_EXIT_W2, "w2"), (T_EXIT_B2, "b2")):
-            self.load_tensor(kind, 0, np.ascontiguousarray(w[name], dtype=np.float32))
+        self.lede_load_weights(exit_qnet=w)
 
     def lede_step_policy(self, n_remaining: int = 1 << 30) -> StepRecord:
         rec = LedeStepRecord()
@@ -389,6 +448,21 @@ class Engine:
                                            n_floats, ctypes.byref(rows), self.stream), self.ctx)
         return out, rows.value
 
+    def lede_debug_logits(self, which: int = LOGITS_VERIFY) -> np.ndarray:
+        """Logits of the last verify / prefill head (LOGITS_VERIFY) or of the
+        last step's draft heads (LOGITS_DRAFT), [rows][vocab]."""
+        V = self.model.vocab
+        out = np.zeros(16 * V, dtype=np.float32)
+        rows = ctypes.c_int32()
+        self._check(self.L.lede_debug_logits(self.ctx, int(which), out.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                             out.size, ctypes.byref(rows), self.stream), self.ctx)
+        return out[:rows.value * V].reshape(rows.value, V)
+
+    def lede_debug_inject_failure(self, n_ops: int):
+        """The (n_ops + 1)-th device operation of the next calls fails with
+        E_HIP before it is issued (one-shot; n_ops < 0 disables)."""
+        self._check(self.L.lede_debug_inject_failure(self.ctx, int(n_ops)), self.ctx)
+
     def lede_prof_enable(self, level: int):
         """0 off, 1 draft / verify phases only, 2 phases and every launch."""
         self._check(self.L.lede_prof_enable(self.ctx, int(level)), self.ctx)
@@ -423,8 +497,12 @@ def op_linear(W, x, use_mfma: bool):
     rc = L.lede_op_repack(dtype, W.data_ptr(), N, K, tiled.data_ptr(), s)
     if rc:
         raise LedeError(rc, "op_repack")
-    rc = L.lede_op_linear(dtype, tiled.data_ptr(), N, K, x.contiguous().data_ptr(), M, y.data_ptr(),
-                          int(use_mfma), s)
+    # rows padded with zeros to the tile width, which the kernels read whole
+    tk = 32 if dtype == 1 else 16
+    ldx = -(-K // tk) * tk
+    xp = torch.zeros(M, ldx, dtype=x.dtype, device=x.device)
+    xp[:, :K] = x
+    rc = L.lede_op_linear(dtype, tiled.data_ptr(), N, K, xp.data_ptr(), ldx, M, y.data_ptr(), int(use_mfma), s)
     if rc:
         raise LedeError(rc, "op_linear")
     return y

@@ -34,6 +34,40 @@ def test_exports_every_declared_symbol(lib):
         assert hasattr(lib, n), n
 
 
+# the boundary's calls, named after the steps of the MDP transition (Section
+# 3.1): weights in, prefill, draft at (l, k), verify, the whole step, KV
+# rollback and state read-back, the logits behind a decision, errors
+BOUNDARY = ["lede_create", "lede_destroy", "lede_last_error", "lede_load_weights", "lede_prefill", "lede_draft",
+            "lede_verify", "lede_step", "lede_truncate", "lede_get_kv_state", "lede_debug_logits"]
+
+
+def test_boundary_calls_declared_and_exported(lib):
+    names = declared_functions()
+    for n in BOUNDARY:
+        assert n in names, n
+        assert hasattr(lib, n), n
+
+
+def test_load_weights_rejects_bad_arguments(lib):
+    from paper_2606_03113_amd import lede
+    assert lib.lede_load_weights(None, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_debug_logits(None, 0, None, 0, None, None) == lede.LEDE_E_ARG
+    assert lib.lede_debug_inject_failure(None, 0) == lede.LEDE_E_ARG
+
+
+def test_weights_struct_matches_header():
+    """The binding's lede_weights mirrors the header's field order and size."""
+    from paper_2606_03113_amd import lede
+    text = open(os.path.join(ROOT, "include", "lede.h")).read()
+    body = re.search(r"typedef struct \{([^{}]*)\} lede_weights;", text).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"\*?\s*(\w+)\s*[,;]", body)
+    assert fields == [f for f, _ in lede.LedeWeights._fields_]
+    assert ctypes.sizeof(lede.LedeWeights) == 3 * 8 + 8 + 8 + 8 * 8
+    assert re.search(r"#define LEDE_LAYER_TENSORS (\d+)", text).group(1) == str(lede.LAYER_TENSORS)
+    assert len(lede.LAYER_ORDER) == lede.LAYER_TENSORS
+
+
 def test_binding_names_match_header():
     from paper_2606_03113_amd import lede
     assert sorted(lede.EXPORTED) == declared_functions()

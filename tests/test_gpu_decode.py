@@ -96,6 +96,35 @@ def test_qnet_policy(model):
     say("  steps=%d subs=%d" % (rep.steps, rep.substitutions))
 
 
+# The Llama-3-8B workload's action grid: exits 2, 4, ..., 32 x lengths 1..8 =
+# 128 actions from a 256-wide hidden layer, more than the Q-network output
+# kernel's one-pass form holds.  A 16-layer model with exits 1..16 has the
+# same grid.
+GRID_128 = shrink(TINY, name="grid128-bf16", n_layers=16, d_model=256, n_heads=4, n_kv_heads=2, head_dim=64,
+                  ffn_dim=688, vocab=1024, dtype="bf16", qnet_hidden=256, exits=tuple(range(1, 17)),
+                  lengths=tuple(range(1, 9)))
+
+
+def test_qnet_policy_128_actions():
+    model = GRID_128
+    assert model.n_actions == 128 and model.qnet_hidden == 256
+    say("qnet policy, 128 actions", model.name)
+    eng, w, q = _engine(model, max_ctx=200)
+    dec = make_decoder(model, w, q, 200)
+    st = SSDState(dec, 4, 64)
+    prompt = _prompt(model)
+    g = eng.lede_prefill(prompt)
+    st.prefill(prompt)
+    rep = Report()
+    if g != st.pending:
+        rep.token(model.dtype, g, dec.head(dec.forward(prompt, 0, model.n_layers)[-1:])[0])
+        eng.lede_set_pending(st.pending)
+    check_ssd(eng, st, model, 40, [(1, 1)], rep, qnet_policy=True)
+    check_ssd(eng, st, model, 60, [(3, 5), (16, 2)], rep, qnet_log=True)
+    say("  steps=%d subs=%d max_err/tol=%.3g" % (rep.steps, rep.substitutions, rep.max_err_rel))
+    assert rep.steps >= 10
+
+
 @pytest.mark.parametrize("model", [TINY_BF16, SMALL_128, SMALL_GQA], ids=lambda m: m.name)
 def test_gpu_ssd_equals_gpu_ar_bitwise(model):
     """Greedy self-speculative output equals greedy autoregressive output on

@@ -44,19 +44,27 @@ def _check(N, K, M, dtype, mfma, seed=0, rows=None):
     assert np.all(err <= tol), "max err %.3g (tol %.3g)" % (err.max(), tol.max())
 
 
+# K past the last whole tile: 688 and 1000 (bf16 tiles of 32 columns), 1000
+# and 40 (fp32 tiles of 16); the tiles' zero padding meets the rows' padding
+RAGGED = [(64, 688), (48, 1000), (16, 40), (256, 11000)]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (64, 1184), (688, 256), (256, 704), (1024, 4096)])
+@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (64, 1184), (688, 256), (256, 704), (1024, 4096)] + RAGGED)
 def test_linear_vec_small(dtype, N, K):
-    if K % (32 if dtype == "bf16" else 16):
-        pytest.skip("K must be a multiple of the tile width")
     _check(N, K, 1, dtype, mfma=False)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("M", [1, 2, 5, 9, 16])
-@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (64, 1184), (256, 704)])
+@pytest.mark.parametrize("N,K", [(16, 32), (48, 96), (64, 1184), (256, 704)] + RAGGED)
 def test_linear_mfma_small(dtype, M, N, K):
     _check(N, K, M, dtype, mfma=True)
+
+
+def test_ragged_k_is_ragged():
+    for N, K in RAGGED:
+        assert K % 32 or K % 16
 
 
 FULL = [
