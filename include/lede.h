@@ -511,6 +511,20 @@ int lede_op_linear(int32_t dtype, const void* tiled, int32_t N, int32_t K, const
  * outside [0, 1). */
 int lede_op_sample(const float* logits, int32_t V, float temperature, float u, int32_t* token, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc): the draws of
+ * lede_op_sample for n_rows rows at once, with no allocation.  Row r is the
+ * device fp32 row logits + r * ld (V used entries, ld >= V), drawn with the
+ * host uniform u[r] in [0, 1); tokens (host, [n_rows]) receives the draws.
+ * The draws' keys live in a library-owned static device array of 32 keys
+ * (2 KiB per device, held until the process ends): n_rows above 32 is
+ * LEDE_E_ARG, as are null pointers, V < 1, ld < V, a temperature that is not
+ * finite and > 0 and a uniform outside [0, 1).  Every call on a device
+ * shares that device's array: calls that overlap on one GPU (other threads,
+ * other streams) race.  Synchronises the stream. */
+int lede_op_sample_noalloc(const float* logits, int32_t n_rows, int32_t ld, int32_t V, float temperature,
+                           const float* u, int32_t* tokens, void* stream);
+
 /* Achievable HBM read bandwidth: reads `bytes` (a multiple of 16, > 0) of the
  * device buffer src once, with the same non-temporal 16-byte loads the
  * linear kernels use for weights, on `grid` (1..65535) blocks of 256 threads;

@@ -6,7 +6,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 SO = os.path.join(HERE, "liblede.so")
-SOURCES = ["linear.hip", "norm.hip", "attention.hip", "accept.hip", "policy.hip", "dqn.hip", "misc.hip", "runtime.cpp",
+SOURCES = ["linear.hip", "norm.hip", "attention.hip", "accept.hip", "policy.hip", "dqn.hip", "misc.hip", "noalloc.hip", "runtime.cpp",
            "dqn.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

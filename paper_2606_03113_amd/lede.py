@@ -83,7 +83,7 @@ EXPORTED = ["lede_region_bytes", "lede_create", "lede_destroy", "lede_last_error
             "lede_get_trace", "lede_set_verify_reuse", "lede_dqn_region_bytes", "lede_dqn_create", "lede_dqn_destroy",
             "lede_dqn_last_error", "lede_dqn_init", "lede_dqn_push", "lede_dqn_record", "lede_dqn_end_episode",
             "lede_dqn_update", "lede_dqn_sync_target", "lede_dqn_act", "lede_dqn_read", "lede_step_submit",
-            "lede_step_collect", "lede_load_weights", "lede_debug_logits", "lede_debug_inject_failure"]
+            "lede_step_collect", "lede_load_weights", "lede_debug_logits", "lede_debug_inject_failure", "lede_op_sample_noalloc"]
 MAX_IN_FLIGHT = 2
 SAMPLE_SLOTS = 16
 SAMPLE_STRIDE = 33
@@ -135,6 +135,7 @@ def load(path: str = LIB_PATH):
     L.lede_step_sampled.argtypes = [vp, P(LedeAction), i32, i32, ctypes.c_float, P(ctypes.c_float), vp,
                                     P(LedeStepRecord)]
     L.lede_op_sample.argtypes = [vp, i32, ctypes.c_float, ctypes.c_float, P(i32), vp]
+    L.lede_op_sample_noalloc.argtypes = [vp, i32, i32, i32, ctypes.c_float, P(ctypes.c_float), P(i32), vp]
     L.lede_step_policy.argtypes = [vp, i32, vp, P(LedeStepRecord)]
     L.lede_set_trace.argtypes = [vp, P(ctypes.c_float), i32, vp]
     L.lede_get_trace.argtypes = [vp, P(ctypes.c_float), P(i32), vp]
@@ -552,6 +553,24 @@ def op_sample(logits, temperature: float, u: float) -> int:
     if rc:
         raise LedeError(rc, "op_sample")
     return tok.value
+
+
+def op_sample_noalloc(logits, temperature: float, u) -> List[int]:
+    """One inverse-CDF draw per row of the float32 GPU tensor logits [rows][V]
+    (rows <= 32) with the uniforms u [rows], through the entry point that
+    allocates nothing."""
+    import torch
+    L = load()
+    x = logits.contiguous()
+    rows, V = x.shape
+    uu = np.ascontiguousarray(u, dtype=np.float32)
+    out = np.zeros(max(rows, 1), dtype=np.int32)
+    s = ctypes.c_void_p(torch.cuda.current_stream(x.device).cuda_stream)
+    rc = L.lede_op_sample_noalloc(x.data_ptr(), rows, V, V, float(temperature),
+                                  uu.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), _i32p(out), s)
+    if rc:
+        raise LedeError(rc, "op_sample_noalloc")
+    return [int(t) for t in out[:rows]]
 
 
 def dqn_noise_count(hidden: int) -> int:
