@@ -57,6 +57,14 @@ def extend_bytes(m, l, c, k):
     return l * m.layer_weight_bytes() + l * (c + k + 1) * m.kv_bytes_per_token_layer()
 
 
+def _span(xs):
+    xs = list(xs)
+    step = xs[1] - xs[0] if len(xs) > 1 else 1
+    if len(xs) > 2 and all(b - a == step for a, b in zip(xs, xs[1:])):
+        return "{%d, %d, ..., %d}" % (xs[0], xs[1], xs[-1])
+    return "{%s}" % ", ".join(map(str, xs))
+
+
 def kernel_source_sha():
     """Hash of the sources the weight-streaming linear kernels are built from."""
     h = hashlib.sha256()
@@ -80,10 +88,11 @@ def traffic_from_profile(kclass, workload, launches):
     return None
 
 
-def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
-    """The CPU oracle on a bounded sample: SSD steps at the workload's action
-    from KV length = prompt length, with the prompt's KV cache filled with
-    synthetic bf16 values instead of an oracle prefill."""
+def cpu_baseline(wl, weights, qnet, prompt_next, policy, actions, budget_s=15.0, max_steps=8):
+    """The CPU oracle on a bounded sample: SSD steps under the bench's policy
+    (fixed action, seeded schedule, or the Q-network's choice) from KV length
+    = prompt length, with the prompt's KV cache filled with synthetic bf16
+    values instead of an oracle prefill."""
     from oracle.model import OracleDecoder, SSDState
     m = wl.model
     P = wl.prompt_len
@@ -96,20 +105,41 @@ def cpu_baseline(wl, weights, qnet, prompt_next, budget_s=15.0, max_steps=8):
     st = SSDState(dec, -(-max_ctx // 64), 64)
     st.pager.ensure(P)
     st.c, st.pending, st.out = P, prompt_next, [prompt_next]
-    l, k = wl.fixed
     t0 = time.time()
     toks = steps = 0
     while steps < max_steps and (steps < 2 or time.time() - t0 < budget_s):
-        rec = st.step(l, k, wl.n_gen, qnet=m.qnet_hidden > 0)
+        l, k = actions[steps % len(actions)]
+        rec = st.step(int(l), int(k), wl.n_gen, qnet=m.qnet_hidden > 0, use_qnet_action=policy == "qnet")
         toks += len(rec.emitted)
         steps += 1
     el = time.time() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": toks / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": "%d SSD steps (l=%d, k=%d) of %s from KV length %d (prompt KV filled with synthetic "
-                      "bf16 values, no oracle prefill); %.1f s" % (steps, l, k, wl.name, P, el),
+            "sample": "%d SSD steps (%s) of %s from KV length %d (prompt KV filled with synthetic "
+                      "bf16 values, no oracle prefill); %.1f s" % (
+                          steps, "Q-network's actions" if policy == "qnet" else
+                          "seeded schedule" if policy == "schedule" else "l=%d, k=%d" % tuple(actions[0]),
+                          wl.name, P, el),
             "host": "%s; %d logical CPUs visible; OMP_NUM_THREADS=%s" % (
                 host_cpu_model(), os.cpu_count() or 0, os.environ.get("OMP_NUM_THREADS", "unset"))}
+
+
+class LazyLayers:
+    """The per-layer weight dicts of a model, generated on access (the
+    70B-shaped model's 138 GB are never all held on the host)."""
+
+    def __init__(self, m):
+        self.m = m
+
+    def __len__(self):
+        return self.m.n_layers
+
+    def __getitem__(self, j):
+        import lede_inputs as li
+        if not 0 <= j < self.m.n_layers:
+            raise IndexError(j)
+        return {n: li.weight_tensor(self.m, n, j) for n in
+                ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")}
 
 
 def host_cpu_model():
@@ -190,8 +220,11 @@ def main():
     ap.add_argument("--in-flight", type=int, default=1,
                     help="forced greedy eager steps: how many are queued on the stream before the oldest "
                          "record is read back (1: one synchronous lede_step at a time)")
-    ap.add_argument("--policy", choices=["fixed", "paper"], default="fixed",
-                    help="paper: the paper's exit policy (seeded random exit Q-network) chooses l* and k per step")
+    ap.add_argument("--policy", choices=["fixed", "qnet", "schedule", "paper"], default=None,
+                    help="how (l*, k) is chosen per step (default: the workload's own): fixed -- the workload's "
+                         "static action (or --l / --k); qnet -- the argmax of the seeded (exit, length) "
+                         "Q-network; schedule -- the workload's seeded uniform schedule; paper -- the paper's exit "
+                         "policy (seeded random exit Q-network)")
     ap.add_argument("--temperature", type=float, default=0.0,
                     help="> 0: speculative sampling at this temperature (uniforms from the seeded generator)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -219,18 +252,36 @@ def main():
         l = args.l if args.l is not None else l
         k = args.k if args.k is not None else k
         wl = replace(wl, fixed=(l, k))
+    policy = args.policy or wl.policy
+    if args.l is not None or args.k is not None:
+        policy = "fixed"
     t0 = time.time()
-    log("generating %s weights ..." % m.name)
-    weights = li.weights(m)
+    # models whose weights would crowd the host are generated layer by layer
+    # while they are loaded (the oracle's CPU baseline then is not run)
+    lazy = m.n_layers * m.layer_weight_bytes() > (60 << 30)
+    log("generating %s weights%s ..." % (m.name, " layer by layer while loading" if lazy else ""))
+    if lazy:
+        weights = {n: li.weight_tensor(m, n) for n in ("embed", "head", "final_norm")}
+        weights["layers"] = LazyLayers(m)
+    else:
+        weights = li.weights(m)
     qnet = li.qnet_weights(m) if m.qnet_hidden else None
     prompt = li.prompt(wl)
     log("  %.1f s" % (time.time() - t0))
-    paper = args.policy == "paper"
+    paper = policy == "paper"
+    sched = li.schedule(wl, wl.n_gen) if policy == "schedule" else None
     if paper and (args.temperature > 0 or args.graphs):
         sys.exit("the exit policy runs greedy, eager steps")
     eng = Engine(m, max_ctx=wl.max_ctx + (16 if paper else 0), k_max=max(12 if paper else 8, k),
                  exit_hidden=16 if paper else 0)
-    eng.load_weights(weights, qnet)
+    if lazy:
+        eng.lede_load_weights({n: weights[n] for n in ("embed", "final_norm", "head")}, qnet)
+        group = max(1, (16 << 30) // m.layer_weight_bytes())
+        for j0 in range(0, m.n_layers, group):
+            eng.lede_load_weights(weights, first_layer=j0, n_layers=min(group, m.n_layers - j0))
+            log("  layers %d..%d loaded  %.1f s" % (j0, min(j0 + group, m.n_layers) - 1, time.time() - t0))
+    else:
+        eng.load_weights(weights, qnet)
     if paper:
         eng.load_exit_qnet(li.exit_qnet_weights(16))
     eng.lede_set_options(args.graphs, 0)
@@ -257,14 +308,21 @@ def main():
 
     n_steps = [0]
 
+    def action():
+        if policy == "schedule":
+            return tuple(int(x) for x in sched[n_steps[0] % len(sched)])
+        return (l, k)
+
     def step():
         if paper:
             rec = eng.lede_step_policy(n_remaining=wl.n_gen - len(produced))
+        elif policy == "qnet":
+            rec = eng.lede_step(None, n_remaining=wl.n_gen - len(produced), log_qnet=False)
         elif args.temperature > 0:
-            rec = eng.lede_step_sampled((l, k), args.temperature, li.step_uniforms(n_steps[0]),
+            rec = eng.lede_step_sampled(action(), args.temperature, li.step_uniforms(n_steps[0]),
                                         n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
         else:
-            rec = eng.lede_step((l, k), n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
+            rec = eng.lede_step(action(), n_remaining=wl.n_gen - len(produced), log_qnet=log_q)
         n_steps[0] += 1
         produced.extend(rec.emitted)
         return rec
@@ -272,7 +330,7 @@ def main():
     from paper_2606_03113_amd.lede import MAX_IN_FLIGHT
     if not 1 <= args.in_flight <= MAX_IN_FLIGHT:
         sys.exit("--in-flight must be in 1..%d" % MAX_IN_FLIGHT)
-    pipelined = (args.in_flight > 1 and not paper and args.temperature == 0 and not args.graphs
+    pipelined = (args.in_flight > 1 and policy == "fixed" and args.temperature == 0 and not args.graphs
                  and not args.verify_reuse)
 
     def run_steps(n):
@@ -446,13 +504,23 @@ def main():
     db = vb = 0.0
     for r in phase_recs:
         c = r.seq_len - r.accepted - 1  # KV length when the step started
-        db += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff)) + (m.qnet_bytes() if log_q else 0)
+        db += sum(pass_bytes(m, r.l, c + i) for i in range(r.k_eff))
+        db += m.qnet_bytes() if (log_q or policy == "qnet") and r.k_eff else 0
         if args.verify_reuse and r.k_eff:
             db += extend_bytes(m, r.l, c, r.k_eff)
             vb += verify_bytes(m, r.k_eff, c, r.l)
         else:
             vb += verify_bytes(m, r.k_eff, c)
     acc_tokens = sum(len(r.emitted) for r in recs)
+    policy_text = {
+        "fixed": "static exit l=%d, draft k=%d%s" % (l, k, ", Q-network logged" if log_q else ""),
+        "qnet": "exit layer and draft length per step from the Q-network (%d->%d->%dx%d) over exits %s x lengths %s"
+                % (m.d_model, m.qnet_hidden, len(m.exits), len(m.lengths), _span(m.exits), _span(m.lengths)),
+        "schedule": "seeded uniform schedule l in %d..%d, k in %d..%d" % (wl.sched_l + wl.sched_k),
+        "paper": "exit layer and draft length per step from the exit policy over exits %s" % (list(m.exits),),
+    }[policy]
+    kv_from = recs[0].seq_len - recs[0].accepted - 1
+    kv_to = recs[-1].seq_len
     accepted = sum(r.accepted for r in recs)
     drafted = sum(r.k_eff for r in recs)
     out = {
@@ -470,19 +538,16 @@ def main():
         "vs_baseline": None,
         "dtype": m.dtype,
         "data": "synthetic (random-init N(0,0.02) weights, uniform-random prompt)",
-        "config": {"workload": "%s: L=%d d=%d heads=%d/%d ffn=%d vocab=%d, prompt %d, generate %d, "
-                               "%s" %
+        "config": {"workload": "%s: L=%d d=%d heads=%d/%d ffn=%d vocab=%d, prompt %d; %s; timed: %d steps "
+                               "from KV length %d to %d (%d tokens) after %d warm-up steps" %
                                (m.name, m.n_layers, m.d_model, m.n_heads, m.n_kv_heads, m.ffn_dim, m.vocab,
-                                wl.prompt_len, wl.n_gen,
-                                "exit layer and draft length per step from the exit policy over exits %s" %
-                                (list(m.exits),) if paper else
-                                "static exit l=%d, draft k=%d, Q-network logged" % (l, k)),
+                                wl.prompt_len, policy_text, args.steps, kv_from, kv_to, acc_tokens, args.warmup),
                    "batch": 1, "prompt_len": wl.prompt_len, "exit_layer": l, "draft_len": k,
                    "graphs": bool(args.graphs), "verify_reuse": bool(args.verify_reuse),
                    "steps_in_flight": args.in_flight if pipelined else 1,
                    "acceptance": ("speculative sampling, T=%g" % args.temperature if args.temperature > 0
                                   else "greedy"),
-                   "policy": "paper exit policy (random exit Q-network)" if paper else "fixed"},
+                   "policy": policy},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": kname,
                      "avg_launch_us": round(1e3 * d["ms"] / max(d["launches"], 1), 3),
@@ -494,6 +559,9 @@ def main():
             "verify_frac": round(vb / (vp["ms"] * 1e6) / HBM_PEAK_GBPS, 4) if vp["ms"] else None,
             "kernel_ms": {n: round(v["ms"] / args.prof_steps, 4) for n, v in prof.items()
                           if not n.endswith("_phase")},
+            "kernel_ms_source": "per step, from an instrumented replay of the same steps with every launch "
+                                "bracketed by its own HIP events (slower than the timed region); phases from a "
+                                "replay with only the draft / verify phases timed",
         },
         "acceptance": {"accepted": accepted, "drafted": drafted,
                        "acc_rate": round(accepted / drafted, 4) if drafted else None,
@@ -516,7 +584,11 @@ def main():
         out["dqn"] = dqn_leg(torch, li)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(wl, weights, qnet, first)
+        if lazy:
+            log("  not run: the weights were generated layer by layer and are not held on the host")
+        else:
+            acts = sched if policy == "schedule" else [(l, k)]
+            out["cpu_baseline"] = cpu_baseline(wl, weights, qnet, first, policy, acts)
         if "dqn" in out:
             out["dqn"]["oracle_updates_per_s"] = dqn_oracle_rate(li)
     print(json.dumps(out), flush=True)
