@@ -1547,6 +1547,8 @@ static int policy_body(lede_ctx* c, int32_t n_remaining, hipStream_t s, lede_ste
   const int k_lim = std::max(0, std::min(std::min(POLICY_MAX_DRAFT, o.k_max), n_remaining - 1));
   int rc;
   if ((rc = ensure_pages(c, c0 + k_lim + 1)) || (rc = upload_table(c, s))) return rc;
+  hipEvent_t ph0 = nullptr;
+  if ((rc = prof_mark(c, s, &ph0, 1))) return rc;
   uint64_t* dk = c->S<uint64_t>(o.dkeys);
   ExitPolicyArgs pa{};
   pa.vocab = o.V; pa.hidden = o.He;
@@ -1601,7 +1603,13 @@ static int policy_body(lede_ctx* c, int32_t n_remaining, hipStream_t s, lede_ste
   }
   const int from = (c->verify_reuse && k > 0) ? l_star : 0;
   if (from && !ran_last && (rc = extend_drafts(c, l_star, k, s))) return rc;
+  // the draft phase includes the decisions' read-backs (the stream idles
+  // while the host waits for each)
+  if (k > 0 && (rc = prof_close(c, s, LEDE_K_DRAFT_PHASE, 0.0, ph0))) return rc;
+  hipEvent_t ph1 = nullptr;
+  if ((rc = prof_mark(c, s, &ph1, 1))) return rc;
   if ((rc = launch_verify(c, k, s, 0.f, from))) return rc;
+  if ((rc = prof_close(c, s, LEDE_K_VERIFY_PHASE, 0.0, ph1))) return rc;
   if ((rc = read_record(c, s))) return rc;
   commit_host(c);
   if ((rc = prof_fold(c))) return rc;

@@ -291,6 +291,9 @@ class Engine:
         def ptr(host):
             if host is None:
                 return None
+            if isinstance(host, self.torch.Tensor) and host.device == self.device:
+                keep.append(host)  # already staged on the device
+                return host.data_ptr()
             d = self._dev(host)
             keep.append(d)
             return d.data_ptr()
