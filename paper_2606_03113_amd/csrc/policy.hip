@@ -5,15 +5,15 @@
 
 namespace lede {
 
-// Keep the POLICY_TOPK largest values seen, in descending order.
+// Keep the POLICY_TOPK largest values seen, in descending order: x bubbles
+// down the list (static indices, no branches).
 __device__ __forceinline__ void top_insert(float (&t)[POLICY_TOPK], float x) {
-  if (!(x > t[POLICY_TOPK - 1])) return;
-  int j = POLICY_TOPK - 1;
-  while (j > 0 && t[j - 1] < x) {
-    t[j] = t[j - 1];
-    --j;
+#pragma unroll
+  for (int j = 0; j < POLICY_TOPK; ++j) {
+    const float hi = fmaxf(t[j], x), lo = fminf(t[j], x);
+    t[j] = hi;
+    x = lo;
   }
-  t[j] = x;
 }
 
 // One block: features (top-k confidence, entropy, trace) of softmax(logits)
@@ -22,44 +22,65 @@ __device__ __forceinline__ void top_insert(float (&t)[POLICY_TOPK], float x) {
 // with m the max logit, e = exp(z - m), S = sum e.
 __global__ __launch_bounds__(SB) void k_exit_policy(ExitPolicyArgs a) {
   __shared__ float red[SW];
-  __shared__ int ired[SW];
-  __shared__ float tops[SB][POLICY_TOPK];
+  __shared__ float tops[SW][POLICY_TOPK];
   __shared__ float hid[SB];
   const float* z = a.logits;
   const int V = a.vocab;
-  const float2 st = row_stats(z, V, 1.f, red);
-  const float m = st.x, S = st.y;
-  const float Wsum = chunk_sum([&](float x, float) { const float d = x - m; return expf(d) * d; }, z, nullptr, V);
-  float wtot;
-  (void)block_excl_scan(Wsum, red, wtot);
-  (void)ired;
-  {  // top-k logits: thread chunks, then 64 lanes over 16 threads each, then one lane
-    float t[POLICY_TOPK];
+  const int C = chunk_len(V), v0 = threadIdx.x * C, v1 = min(V, v0 + C);
+  // pass 1 over this thread's chunk (batched loads): the max and the top k
+  float m = -INFINITY;
+  float t[POLICY_TOPK];
 #pragma unroll
-    for (int j = 0; j < POLICY_TOPK; ++j) t[j] = -INFINITY;
-    const int C = chunk_len(V), v0 = threadIdx.x * C, v1 = min(V, v0 + C);
-    for (int v = v0; v < v1; ++v) top_insert(t, z[v]);
+  for (int j = 0; j < POLICY_TOPK; ++j) t[j] = -INFINITY;
+  for (int b = v0; b < v1; b += CB) {
+    float r[CB];
+    load_batch(z, v1, b, r);
 #pragma unroll
-    for (int j = 0; j < POLICY_TOPK; ++j) tops[threadIdx.x][j] = t[j];
-    __syncthreads();
-    if (threadIdx.x < 64) {
-#pragma unroll
-      for (int j = 0; j < POLICY_TOPK; ++j) t[j] = -INFINITY;
-      for (int i = 0; i < SB / 64; ++i)
-        for (int j = 0; j < POLICY_TOPK; ++j) top_insert(t, tops[threadIdx.x * (SB / 64) + i][j]);
+    for (int j = 0; j < CB; ++j) {
+      const float x = b + j < v1 ? r[j] : -INFINITY;
+      m = fmaxf(m, x);
+      top_insert(t, x);
     }
-    __syncthreads();
-    if (threadIdx.x < 64)
-#pragma unroll
-      for (int j = 0; j < POLICY_TOPK; ++j) tops[threadIdx.x][j] = t[j];
-    __syncthreads();
   }
+  m = block_max_f(m, red);
+  // the top-k lists of a wavefront merged pairwise through shuffles, then
+  // the waves' lists by one thread below
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    float u[POLICY_TOPK];
+#pragma unroll
+    for (int j = 0; j < POLICY_TOPK; ++j) u[j] = __shfl_xor(t[j], o);
+#pragma unroll
+    for (int j = 0; j < POLICY_TOPK; ++j) top_insert(t, u[j]);
+  }
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int j = 0; j < POLICY_TOPK; ++j) tops[threadIdx.x >> 6][j] = t[j];
+  // pass 2: S = sum e and W = sum e (z - m), each in index order
+  float s_e = 0.f, s_w = 0.f;
+  for (int b = v0; b < v1; b += CB) {
+    float r[CB];
+    load_batch(z, v1, b, r);
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
+      if (b + j < v1) {
+        const float d = r[j] - m, e = expf(d);
+        s_e += e;
+        s_w += e * d;
+      }
+  }
+  float S, wtot;
+  (void)block_excl_scan(s_e, red, S);
+  __syncthreads();
+  (void)block_excl_scan(s_w, red, wtot);
+  __syncthreads();
   __shared__ float state[3];
   if (threadIdx.x == 0) {
     float t[POLICY_TOPK];
 #pragma unroll
     for (int j = 0; j < POLICY_TOPK; ++j) t[j] = -INFINITY;
-    for (int i = 0; i < 64; ++i)
+    for (int i = 0; i < SW; ++i)
+#pragma unroll
       for (int j = 0; j < POLICY_TOPK; ++j) top_insert(t, tops[i][j]);
     const int kk = min(POLICY_TOPK, V);
     float ts = 0.f;
