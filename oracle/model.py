@@ -221,12 +221,21 @@ def argmax_info(z: np.ndarray) -> ArgmaxInfo:
 @dataclass
 class Tolerance:
     """Logit tolerance: absolute for fp32 models, relative to the row's logit
-    range for bf16 models."""
+    range for bf16 models.  The bf16 bound is set for the depths of the
+    paper's models (Section 4.1: LLaMA-2 7B and 13B, up to 40 layers).  A
+    deeper bf16 model accumulates more rounding decisions that the fp32 GPU
+    path and the fp64 oracle take differently at the same bf16 quantisation
+    points, and the logit difference grows about as the square root of the
+    depth, so past ref_depth layers the bound scales by sqrt(depth /
+    ref_depth)."""
     abs_f32: float = 1e-4
     rel_bf16: float = 2e-2
+    ref_depth: int = 40
 
-    def of(self, dtype: str, span: float) -> float:
-        return self.abs_f32 if dtype == "f32" else self.rel_bf16 * span
+    def of(self, dtype: str, span: float, depth: int = 0) -> float:
+        if dtype == "f32":
+            return self.abs_f32
+        return self.rel_bf16 * span * math.sqrt(max(1.0, depth / self.ref_depth))
 
 
 def accept_length(drafts: Sequence[int], verify: Sequence[int]) -> int:

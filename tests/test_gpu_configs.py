@@ -13,7 +13,18 @@ prefill stays within a minute:
 
 Each case: prefill logits, then self-speculative steps against the oracle
 (every draft row, every verify row up to the acceptance point, acceptance,
-KV length, page table), and greedy SSD == greedy AR on the GPU."""
+KV length, page table), and greedy SSD == greedy AR on the GPU.
+
+The same shapes also run at full depth (32, 40 and 80 layers) with the
+workloads' own action sets: the Llama-3-8B Q-network over its real grid
+(16 exits x 8 lengths = 128 actions), the seeded schedules l 5..20 (13B) and
+l 10..40 (70B).  There the prompts are short and four generated layer
+weight sets (two for the 70B shape) repeat over the depth (layer j uses set
+j mod 4, on the GPU and in the oracle alike), so that host generation and
+the oracle's fp64 passes stay within minutes; every layer still has its own
+KV cache, exit index and weights in the arena.  The 80-layer shape is past
+the depths of the paper's models: its bf16 bound scales by sqrt(80 / 40)
+(oracle.model.Tolerance)."""
 import time
 
 import numpy as np
@@ -101,3 +112,55 @@ def test_config_shape_parity(case):
         out += rec.emitted
         i += 1
     assert out == ar
+
+
+FULL = {
+    "llama3-8b-L32": dict(wl="llama3-8b", prompt=16, n_total=10, distinct=4),
+    "llama2-13b-L40": dict(wl="llama2-13b", prompt=16, n_total=8, distinct=4),
+    "llama2-70b-L80": dict(wl="llama2-70b", prompt=8, n_total=4, distinct=2),
+}
+
+
+@pytest.mark.parametrize("case", list(FULL))
+def test_config_full_depth_parity(case):
+    from paper_2606_03113_amd import Engine
+    spec = FULL[case]
+    wl = WORKLOADS[spec["wl"]]
+    m = wl.model
+    t = time.time()
+    nd = spec["distinct"]
+    w4 = li.weights(shrink(m, n_layers=nd))
+    w = dict(w4, layers=[w4["layers"][j % nd] for j in range(m.n_layers)])
+    q = li.qnet_weights(m)
+    prompt = li.prompt(wl, length=spec["prompt"])
+    say("%s: %d layers (%d distinct), %d actions, weights %.1f s, prompt %d" %
+        (case, m.n_layers, nd, m.n_actions, time.time() - t, len(prompt)))
+    max_ctx = len(prompt) + 48
+    eng = Engine(m, max_ctx=max_ctx, k_max=8)
+    t = time.time()
+    eng.load_weights(w, q)
+    say("  loaded in %.1f s" % (time.time() - t))
+    eng.lede_set_options(0, 1)
+    g = eng.lede_prefill(prompt)
+    dec = OracleDecoder(m, w, max_ctx, q)
+    st = SSDState(dec, -(-max_ctx // 64), 64)
+    t = time.time()
+    st.pager.ensure(len(prompt))
+    z = dec.head(dec.forward(prompt, 0, m.n_layers)[-1:])[0]
+    info = argmax_info(z)
+    st.c, st.pending, st.out = len(prompt), info.token, [info.token]
+    say("  oracle prefill %.1f s" % (time.time() - t))
+    rep = Report(depth=m.n_layers)
+    rep.row(m.dtype, eng.logits(0)[-1], z)
+    if not rep.token(m.dtype, g, z):
+        eng.lede_set_pending(st.pending)
+    t = time.time()
+    if wl.policy == "qnet":
+        check_ssd(eng, st, m, spec["n_total"], [(1, 1)], rep, qnet_policy=True)
+    else:
+        sched = np.stack([li.uniform_int(li.SEED_SCHEDULE, li.STREAM_SCHED_L, 64, *wl.sched_l),
+                          li.uniform_int(li.SEED_SCHEDULE, li.STREAM_SCHED_K, 64, *wl.sched_k)], 1)
+        check_ssd(eng, st, m, spec["n_total"], sched, rep)
+    say("  steps=%d rows=%d max_err/tol=%.3g max_abs=%.3g substitutions=%d  %.1f s" %
+        (rep.steps, rep.rows, rep.max_err_rel, rep.max_err_abs, rep.substitutions, time.time() - t))
+    assert rep.steps >= 2

@@ -48,3 +48,16 @@ def test_near_tie_bound_is_the_poisson_quantile():
         assert stats.poisson.sf(n, mu) <= 1e-3
         if n > 0:
             assert stats.poisson.sf(n - 1, mu) > 1e-3
+
+
+def test_bf16_tolerance_scales_only_past_the_papers_depths():
+    """The bf16 bound is the stated 2e-2 of the logit range for models of up to
+    40 layers (the paper's LLaMA-2 7B / 13B); deeper ones get sqrt(depth / 40)
+    of it; fp32 stays absolute."""
+    from oracle.model import Tolerance
+    t = Tolerance()
+    for depth in (0, 4, 32, 40):
+        assert t.of("bf16", 10.0, depth) == pytest.approx(0.2)
+    assert t.of("bf16", 10.0, 80) == pytest.approx(0.2 * 2 ** 0.5)
+    assert t.of("bf16", 10.0, 160) == pytest.approx(0.4)
+    assert t.of("f32", 10.0, 80) == 1e-4
