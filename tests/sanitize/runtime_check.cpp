@@ -3,7 +3,14 @@
 // Without a GPU it drives what the host does on its own: region sizing over
 // the supported shapes and the rejected ones, argument checks of every entry
 // point, and context creation failing cleanly when the device calls do.
+// With a GPU it also decodes on a tiny fp32 model whose KV pool holds four
+// pages, so that the host's pager, rollback and pipelining paths run: prefill,
+// forced, Q-network, sampled and exit-policy steps, truncation and resume, a
+// permuted free list, injected failures (the state must come back
+// unchanged), two steps in flight, and the pool and context running out.
 // Exit status 0 when everything ran clean and returned the documented codes.
+#include <hip/hip_runtime.h>
+
 #include <cstdio>
 #include <cstring>
 #include <vector>
@@ -33,6 +40,151 @@ static lede_config config(int L, int d, int nq, int nkv, int hd, int F, int V, i
   return c;
 }
 
+
+// ---- with a GPU: a tiny fp32 model through the decoding state machine ---------
+
+struct KvState {
+  int32_t seq_len = 0, pending = 0, n_table = 0;
+  std::vector<int32_t> table = std::vector<int32_t>(64, -7);
+  bool operator==(const KvState& o) const {
+    return seq_len == o.seq_len && pending == o.pending && n_table == o.n_table &&
+           std::vector<int32_t>(table.begin(), table.begin() + n_table) ==
+               std::vector<int32_t>(o.table.begin(), o.table.begin() + o.n_table);
+  }
+};
+static KvState kv_state(lede_ctx* ctx) {
+  KvState k;
+  EXPECT(lede_get_kv_state(ctx, &k.seq_len, &k.pending, k.table.data(), 64, &k.n_table) == LEDE_OK);
+  return k;
+}
+
+static uint32_t rng = 88172645u;
+static float frand() {
+  rng ^= rng << 13;
+  rng ^= rng >> 17;
+  rng ^= rng << 5;
+  return (float)((rng >> 8) / 8388608.0 - 1.0);
+}
+
+static void decode_on_gpu(lede_ctx* ctx, const lede_config& c) {
+  // weights: one device buffer per tensor, random values
+  const int d = c.d_model, qd = c.n_heads * c.head_dim, kvd = c.n_kv_heads * c.head_dim, F = c.ffn_dim, V = c.vocab;
+  const int A = c.n_exits * c.n_lengths, H = c.qnet_hidden, He = c.exit_qnet_hidden;
+  std::vector<void*> bufs;
+  auto load = [&](int kind, int layer, size_t n, float scale, float offset) {
+    std::vector<float> h(n);
+    for (float& x : h) x = offset + scale * frand();
+    void* dv = nullptr;
+    EXPECT(hipMalloc(&dv, n * 4) == hipSuccess);
+    EXPECT(hipMemcpy(dv, h.data(), n * 4, hipMemcpyHostToDevice) == hipSuccess);
+    bufs.push_back(dv);
+    EXPECT(lede_load_tensor(ctx, kind, layer, dv, nullptr) == LEDE_OK);
+  };
+  load(LEDE_T_EMBED, 0, (size_t)V * d, 1.f, 0.f);
+  load(LEDE_T_FINAL_NORM, 0, d, 0.1f, 1.f);
+  load(LEDE_T_HEAD, 0, (size_t)V * d, 0.05f, 0.f);
+  for (int l = 0; l < c.n_layers; ++l) {
+    load(LEDE_T_ATTN_NORM, l, d, 0.1f, 1.f);
+    load(LEDE_T_WQ, l, (size_t)qd * d, 0.05f, 0.f);
+    load(LEDE_T_WK, l, (size_t)kvd * d, 0.05f, 0.f);
+    load(LEDE_T_WV, l, (size_t)kvd * d, 0.05f, 0.f);
+    load(LEDE_T_WO, l, (size_t)d * qd, 0.05f, 0.f);
+    load(LEDE_T_FFN_NORM, l, d, 0.1f, 1.f);
+    load(LEDE_T_WG, l, (size_t)F * d, 0.05f, 0.f);
+    load(LEDE_T_WU, l, (size_t)F * d, 0.05f, 0.f);
+    load(LEDE_T_WD, l, (size_t)d * F, 0.05f, 0.f);
+  }
+  load(LEDE_T_QNET_W1, 0, (size_t)H * d, 0.05f, 0.f);
+  load(LEDE_T_QNET_B1, 0, H, 0.f, 0.f);
+  load(LEDE_T_QNET_W2, 0, (size_t)A * H, 0.05f, 0.f);
+  load(LEDE_T_QNET_B2, 0, A, 0.f, 0.f);
+  load(LEDE_T_EXIT_W1, 0, (size_t)He * 3, 0.5f, 0.f);
+  load(LEDE_T_EXIT_B1, 0, He, 0.5f, 0.f);
+  load(LEDE_T_EXIT_W2, 0, (size_t)2 * He, 0.5f, 0.f);
+  load(LEDE_T_EXIT_B2, 0, 2, 0.f, 0.f);
+  EXPECT(hipDeviceSynchronize() == hipSuccess);
+
+  // a permuted free list, then a prompt over two pages
+  const int32_t order[4] = {2, 0, 3, 1};
+  EXPECT(lede_set_free_list(ctx, order, 4) == LEDE_OK);
+  std::vector<int32_t> prompt(70);
+  for (size_t i = 0; i < prompt.size(); ++i) prompt[i] = (int32_t)((i * 37 + 11) % V);
+  int32_t next = -1;
+  EXPECT(lede_prefill(ctx, prompt.data(), (int32_t)prompt.size(), nullptr, &next) == LEDE_OK);
+  EXPECT(next >= 0 && next < V);
+  KvState k0 = kv_state(ctx);
+  EXPECT(k0.seq_len == 70 && k0.n_table == 2 && k0.table[0] == 2 && k0.table[1] == 0);
+  EXPECT(lede_set_free_list(ctx, order, 4) == LEDE_E_STATE);  // pages are allocated
+
+  lede_step_record rec;
+  float unif[LEDE_SAMPLE_STRIDE];
+  for (float& u : unif) u = 0.5f * (frand() + 1.f) * 0.999f;
+  for (int i = 0; i < 6; ++i) {
+    lede_action act = {1 + i % c.n_layers, 1 + i % 5};
+    EXPECT(lede_step(ctx, &act, i & 1, 40, nullptr, &rec) == LEDE_OK);
+    EXPECT(rec.n_emitted == rec.accepted + 1 && rec.seq_len == kv_state(ctx).seq_len);
+  }
+  EXPECT(lede_step(ctx, nullptr, 0, 40, nullptr, &rec) == LEDE_OK);           // the Q-network's action
+  EXPECT(lede_step_sampled(ctx, nullptr, 0, 40, 0.6f, unif, nullptr, &rec) == LEDE_OK);
+  EXPECT(lede_step_policy(ctx, 40, nullptr, &rec) == LEDE_OK);                // the paper's exit policy
+  float trace[20];
+  int32_t n_trace = 0;
+  EXPECT(lede_get_trace(ctx, trace, &n_trace, nullptr) == LEDE_OK && n_trace > 0);
+
+  // injected failures: every operation index of a forced step, state unchanged
+  for (int n_ops = 1; n_ops <= 12; ++n_ops) {
+    const KvState before = kv_state(ctx);
+    EXPECT(lede_debug_inject_failure(ctx, n_ops) == LEDE_OK);
+    lede_action act = {2, 4};
+    const int rc = lede_step(ctx, &act, 1, 40, nullptr, &rec);
+    EXPECT(rc == LEDE_OK || rc == LEDE_E_HIP);
+    if (rc != LEDE_OK) EXPECT(kv_state(ctx) == before);
+    EXPECT(lede_debug_inject_failure(ctx, -1) == LEDE_OK);
+  }
+
+  // two steps in flight
+  {
+    lede_action act = {1, 3};
+    EXPECT(lede_step_submit(ctx, &act, 0, 40, nullptr) == LEDE_OK);
+    EXPECT(lede_step_submit(ctx, &act, 0, 40, nullptr) == LEDE_OK);
+    EXPECT(lede_step_submit(ctx, &act, 0, 40, nullptr) == LEDE_E_STATE);
+    EXPECT(lede_step(ctx, &act, 0, 40, nullptr, &rec) == LEDE_E_STATE);
+    EXPECT(lede_step_collect(ctx, nullptr, &rec) == LEDE_OK);
+    EXPECT(lede_step_collect(ctx, nullptr, &rec) == LEDE_OK);
+    EXPECT(lede_step_collect(ctx, nullptr, &rec) == LEDE_E_STATE);
+  }
+
+  // draft, truncate (discards it) and resume by re-prefill
+  {
+    int32_t drafts[4];
+    const KvState before = kv_state(ctx);
+    EXPECT(lede_draft(ctx, 2, 4, nullptr, drafts) == LEDE_OK);
+    EXPECT(lede_draft(ctx, 2, 4, nullptr, drafts) == LEDE_E_STATE);
+    EXPECT(lede_truncate(ctx, before.seq_len - 5, nullptr) == LEDE_OK);
+    EXPECT(lede_truncate(ctx, before.seq_len, nullptr) == LEDE_E_ARG);
+    EXPECT(lede_prefill(ctx, prompt.data(), 5, nullptr, &next) == LEDE_OK);
+    EXPECT(kv_state(ctx).seq_len == before.seq_len);
+  }
+
+  // the pool (4 pages = 256 positions) and the context (max_ctx) run out
+  {
+    int rc = LEDE_OK;
+    for (int i = 0; i < 400 && rc == LEDE_OK; ++i) {
+      const KvState before = kv_state(ctx);
+      lede_action act = {2, 8};
+      rc = lede_step(ctx, &act, 0, 100, nullptr, &rec);
+      if (rc != LEDE_OK) EXPECT(kv_state(ctx) == before);
+    }
+    EXPECT(rc == LEDE_E_KV_FULL || rc == LEDE_E_CTX_OVERFLOW);
+    EXPECT(lede_truncate(ctx, 0, nullptr) == LEDE_OK && kv_state(ctx).n_table == 0);
+    std::vector<int32_t> big(300, 5);
+    EXPECT(lede_prefill(ctx, big.data(), (int32_t)big.size(), nullptr, &next) == LEDE_E_KV_FULL ||
+           lede_prefill(ctx, big.data(), (int32_t)big.size(), nullptr, &next) == LEDE_E_CTX_OVERFLOW);
+    EXPECT(kv_state(ctx).seq_len == 0);
+  }
+  for (void* b : bufs) (void)hipFree(b);
+}
+
 int main() {
   // region sizes of the supported shapes
   const lede_config shapes[] = {config(4, 256, 4, 4, 64, 688, 1024, LEDE_DTYPE_F32),
@@ -60,8 +212,7 @@ int main() {
     EXPECT(lede_region_bytes(&c, nullptr, nullptr, nullptr) == LEDE_E_UNSUPPORTED);
     EXPECT(lede_region_bytes(nullptr, nullptr, nullptr, nullptr) == LEDE_E_ARG);
   }
-  // context creation: bad arguments, then a valid request whose device
-  // calls fail without a GPU (the partly built context is torn down)
+  // context creation: bad arguments, then a valid request
   {
     const lede_config& c = shapes[0];
     size_t wb = 0, kvb = 0, wsb = 0;
@@ -75,11 +226,31 @@ int main() {
     EXPECT(lede_create(nullptr, al(w), wb, al(kv), kvb, al(ws), wsb, &ctx) == LEDE_E_ARG && ctx == nullptr);
     EXPECT(lede_create(&c, al(w), wb - 1, al(kv), kvb, al(ws), wsb, &ctx) == LEDE_E_ARG);
     EXPECT(lede_create(&c, (unsigned char*)al(w) + 16, wb, al(kv), kvb, al(ws), wsb, &ctx) == LEDE_E_ARG);
-    const int rc = lede_create(&c, al(w), wb, al(kv), kvb, al(ws), wsb, &ctx);
-    if (rc == LEDE_OK) {
-      lede_destroy(ctx);  // a GPU is present after all
-    } else {
+    int n_dev = 0;
+    if (hipGetDeviceCount(&n_dev) != hipSuccess || n_dev == 0) {
+      // no GPU: the first device call of a valid request fails and the partly
+      // built context is torn down (with a GPU, host buffers are never passed)
+      const int rc = lede_create(&c, al(w), wb, al(kv), kvb, al(ws), wsb, &ctx);
       EXPECT(rc == LEDE_E_HIP && ctx == nullptr);
+    } else {
+      // a GPU: the same shape over device regions, with a four-page KV pool
+      lede_config g = c;
+      g.n_pages = 4;
+      g.max_ctx = 300;
+      EXPECT(lede_region_bytes(&g, &wb, &kvb, &wsb) == LEDE_OK);
+      void *dw = nullptr, *dkv = nullptr, *dws = nullptr;
+      EXPECT(hipMalloc(&dw, wb) == hipSuccess && hipMalloc(&dkv, kvb) == hipSuccess &&
+             hipMalloc(&dws, wsb) == hipSuccess);
+      lede_ctx* gctx = nullptr;
+      EXPECT(lede_create(&g, dw, wb, dkv, kvb, dws, wsb, &gctx) == LEDE_OK);
+      if (gctx) {
+        decode_on_gpu(gctx, g);
+        lede_destroy(gctx);
+        std::printf("decoded on the GPU\n");
+      }
+      (void)hipFree(dw);
+      (void)hipFree(dkv);
+      (void)hipFree(dws);
     }
   }
   // every context entry point rejects a null context
