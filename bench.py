@@ -125,8 +125,16 @@ def cpu_baseline(wl, weights, qnet, prompt_next, policy, actions, budget_s=15.0,
         toks += len(rec.emitted)
         steps += 1
     el = time.time() - t0
+    # plain autoregressive steps of the oracle on the same state (k = 0)
+    t1 = time.time()
+    ar_toks = 0
+    while ar_toks < 2 or (ar_toks < max_steps and time.time() - t1 < budget_s / 3):
+        ar_toks += len(st.step(1, 0, wl.n_gen).emitted)
+    ar_el = time.time() - t1
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": toks / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "ar_value": ar_toks / ar_el, "ar_sample": "%d autoregressive steps after the SSD sample; %.1f s" % (
+                ar_toks, ar_el),
             "sample": "%d SSD steps (%s) of %s from KV length %d (prompt KV filled with synthetic "
                       "bf16 values, no oracle prefill); %.1f s" % (
                           steps, "Q-network's actions" if policy == "qnet" else

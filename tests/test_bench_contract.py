@@ -40,6 +40,7 @@ def test_bench_line_on_the_tiny_workload():
     assert abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-3 and rf["kernel"].startswith("lede::k_linear<0,")
     cb = d["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["value"] > 0 and cb["cores"] >= 1 and cb["sample"]
+    assert cb["ar_value"] > 0 and cb["ar_sample"]
     # value: committed tokens (a + 1 per step) over the timed steps
     tokens = d["acceptance"]["accepted"] + d["steps"]
     assert abs(d["value"] - tokens * 1e3 / (d["ms_per_step"] * d["steps"])) <= 0.01 * d["value"]
