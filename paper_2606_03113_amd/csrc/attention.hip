@@ -5,6 +5,10 @@ namespace lede {
 
 // ---- attention over the paged KV cache --------------------------------------
 
+// At most this many thread groups in the combine kernel (16 pages each per
+// round of loads); a launch uses ceil(max_chunks / 16) of them.
+constexpr int COMBINE_GROUPS = 8;
+
 // Eight consecutive cache elements as fp32.
 template <int DT>
 __device__ __forceinline__ void load8(const void* base, size_t idx, float* o) {
@@ -145,15 +149,32 @@ __global__ __launch_bounds__(256) void k_attn_partial(AttnArgs a) {
   }
 }
 
-// Combine the per-page partials of every (row, head) in page order, 16
-// pages per round trip: the loads are unconditional (a page index past the
-// buffer is clamped to its last page, and pages past the row's position are
-// loaded but not folded), so they issue together instead of one guarded
-// load after another, and the first 16 go out with the sequence length.
+// One step of the page-ordered combine: fold a page's (max, sum, weighted
+// value) into the running (mx, l, acc).
+__device__ __forceinline__ void fold_step(float& mx, float& l, float& acc, float pm, float pl, float pa) {
+  const float nm = fmaxf(mx, pm);
+  const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
+  const float sn = __expf(pm - nm);
+  l = l * so + pl * sn;
+  acc = acc * so + pa * sn;
+  mx = nm;
+}
+
+// Combine the per-page partials of every (row, head): S = blockDim / HD
+// groups of HD threads, group s folding pages 16 s .. 16 s + 15 (then
+// 16 s + 16 S, ...) in page order, one thread per dim; the groups' running
+// states are then folded in group order.  Up to 16 pages only group 0 has
+// pages and the result is the plain page-ordered fold.  The loads are
+// unconditional (a page index past the buffer is clamped to its last page,
+// and pages past the row's position are loaded but not folded), so each
+// group's 16 issue together, and before the sequence length arrives.
 template <int DT, int HD>
-__global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
+__global__ __launch_bounds__(HD * COMBINE_GROUPS) void k_attn_combine(AttnArgs a) {
   constexpr int B = 16;
-  const int m = blockIdx.x / a.nq, head = blockIdx.x % a.nq, i = threadIdx.x;
+  __shared__ float st[COMBINE_GROUPS][3][HD];
+  const int S = blockDim.x / HD;
+  const int m = blockIdx.x / a.nq, head = blockIdx.x % a.nq;
+  const int i = threadIdx.x % HD, sg = threadIdx.x / HD;
   const float* p = a.part + ((size_t)m * a.nq + head) * a.max_chunks * (HD + 2);
   float pm[B], pl[B], pa[B];
   auto load = [&](int j0) {
@@ -165,25 +186,24 @@ __global__ __launch_bounds__(HD) void k_attn_combine(AttnArgs a) {
       pa[u] = q[2 + i];
     }
   };
-  load(0);
+  load(sg * B);
   const int pos = *a.seq_len + a.pos_off + m;
   const int nc = pos / 64 + 1;
-  __builtin_assume(nc >= 1);  // lets the first loads issue before the length arrives
   float mx = -INFINITY, l = 0.f, acc = 0.f;
-  for (int j0 = 0; j0 < nc; j0 += B) {
-    if (j0 > 0) load(j0);
+  for (int j0 = sg * B; j0 < nc; j0 += S * B) {
+    if (j0 > sg * B) load(j0);
 #pragma unroll
-    for (int u = 0; u < B; ++u) {
-      if (j0 + u >= nc) break;
-      const float nm = fmaxf(mx, pm[u]);
-      const float so = (mx == -INFINITY) ? 0.f : __expf(mx - nm);
-      const float sn = __expf(pm[u] - nm);
-      l = l * so + pl[u] * sn;
-      acc = acc * so + pa[u] * sn;
-      mx = nm;
-    }
+    for (int u = 0; u < B; ++u)
+      if (j0 + u < nc) fold_step(mx, l, acc, pm[u], pl[u], pa[u]);
   }
-  Elem<DT>::store(a.out, (size_t)m * a.ldo + head * HD + i, acc / l);
+  st[sg][0][i] = mx;
+  st[sg][1][i] = l;
+  st[sg][2][i] = acc;
+  __syncthreads();
+  if (sg == 0) {
+    for (int q = 1; q < S && q * B < nc; ++q) fold_step(mx, l, acc, st[q][0][i], st[q][1][i], st[q][2][i]);
+    Elem<DT>::store(a.out, (size_t)m * a.ldo + head * HD + i, acc / l);
+  }
 }
 
 // Eight fp32 values as bf16 high parts and the bf16 rounding of what is left,
@@ -372,23 +392,24 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, hipStream_t s) {
   const int n_rs = (a.M * G + a.rows_per_block - 1) / a.rows_per_block;
   dim3 grid(a.nkv * n_rs, a.n_split);
   const int combine_grid = a.M * a.nq;
+  const int groups = (a.max_chunks + 15) / 16 < COMBINE_GROUPS ? (a.max_chunks + 15) / 16 : COMBINE_GROUPS;
   if (dtype == 1) {
     if (a.hd == 128) {
       if (a.mfma) hipLaunchKernelGGL((k_attn_mfma<128>), grid, dim3(256), 0, s, a);
       else hipLaunchKernelGGL((k_attn_partial<1, 128>), grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL((k_attn_combine<1, 128>), dim3(combine_grid), dim3(128), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<1, 128>), dim3(combine_grid), dim3(128 * groups), 0, s, a);
     } else {
       if (a.mfma) hipLaunchKernelGGL((k_attn_mfma<64>), grid, dim3(256), 0, s, a);
       else hipLaunchKernelGGL((k_attn_partial<1, 64>), grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL((k_attn_combine<1, 64>), dim3(combine_grid), dim3(64), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<1, 64>), dim3(combine_grid), dim3(64 * groups), 0, s, a);
     }
   } else {
     if (a.hd == 128) {
       hipLaunchKernelGGL((k_attn_partial<0, 128>), grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL((k_attn_combine<0, 128>), dim3(combine_grid), dim3(128), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<0, 128>), dim3(combine_grid), dim3(128 * groups), 0, s, a);
     } else {
       hipLaunchKernelGGL((k_attn_partial<0, 64>), grid, dim3(256), 0, s, a);
-      hipLaunchKernelGGL((k_attn_combine<0, 64>), dim3(combine_grid), dim3(64), 0, s, a);
+      hipLaunchKernelGGL((k_attn_combine<0, 64>), dim3(combine_grid), dim3(64 * groups), 0, s, a);
     }
   }
   return hipGetLastError();

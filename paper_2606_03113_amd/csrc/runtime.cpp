@@ -551,7 +551,11 @@ int run_layers(lede_ctx* c, int M, bool vec, TokenSrc tok, int pos_off, int l_be
     const int G = o.nq / o.nkv;
     at.rows_per_block = std::min(16, M * G);
     const int n_rs = (M * G + at.rows_per_block - 1) / at.rows_per_block;
-    at.n_split = std::max(1, std::min(o.max_chunks, (512 + o.nkv * n_rs - 1) / (o.nkv * n_rs)));
+    // about 2048 blocks, one page each where the context allows: at 4096
+    // positions (13B shape, 65 pages per head) 16.05 against 16.32 ms per
+    // step with 512 blocks of five pages; shorter contexts have a page per
+    // block either way
+    at.n_split = std::max(1, std::min(o.max_chunks, (2048 + o.nkv * n_rs - 1) / (o.nkv * n_rs)));
     at.max_chunks = o.max_chunks;
     at.part = c->S<float>(o.part);
     at.out = c->S<void>(o.attn_out); at.ldo = o.qd;
