@@ -230,8 +230,10 @@ __device__ __forceinline__ void split8(const float* x, uint4& hi, uint4& lo) {
 // same way; the wavefront's value columns are staged in LDS and read back
 // transposed).  Every output element is a fixed-order function of its own
 // row, so a row's partials do not depend on the rows sharing its block.
+// Five waves per SIMD (at most 96 VGPRs, no spills) keeps five blocks per
+// CU instead of four.
 template <int HD>
-__global__ __launch_bounds__(256) void k_attn_mfma(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_attn_mfma(AttnArgs a) {
   constexpr int KS = HD / 32;          // k-steps of the scores
   constexpr int DW = HD / 4;           // output dims per wavefront
   constexpr int DT = DW / 16;          // 16-dim output tiles per wavefront
